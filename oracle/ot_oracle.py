@@ -1,0 +1,276 @@
+"""CPU oracle for OutlierTune's per-channel-quantized linear layer.
+
+TEST INFRASTRUCTURE ONLY.  This module is the parity reference that the HIP
+library is checked against.  Only the test suite, the package's smoke check
+and the benchmark's CPU-baseline leg may import it; the product path never
+calls it and shares no code with it.
+
+It is written for obviousness, not speed: plain numpy, float64 wherever the
+method leaves the precision open, every rounding spelled out.  The paper
+(OutlierTune, Wang et al., 2024) fixes the algebra; where it leaves a choice
+open the reading taken here is noted at the function that makes it.
+
+Notation follows the paper.  X is [M x K] (tokens x input channels), the
+linear's weight W is stored as nn.Linear stores it, [N x K] (so the paper's
+W^T is its transpose), b is [N].  ``qa`` and ``qw`` are the largest codes of
+the activation and weight quantizers, 2^(bits-1) - 1 (symmetric, signed).
+
+Functions and the passages they follow
+--------------------------------------
+calibrate       Sec. 3.2 (symmetrization factor z from per-channel max/min)
+                and App. A (static min-max calibration of activations).
+fold_weights    Sec. 3.1, Eq. (e) (W_s = W scaled by s^X along input
+                channels), Eq. (f) (per-output-channel quantization of W_s),
+                Sec. 3.2, Eq. (g) (shift z moved into the bias: z W^T + b),
+                and the Implementation paragraph (weights quantized offline).
+quantize_act    Eq. (g): round((X - z) / s^X), per input channel.
+int_gemm        Eq. (f) right-hand side: the integer sum over k.
+epilogue        Eq. (g): scale by s^{W_s}_j, then add (z W^T + b).
+qlinear         int_gemm followed by epilogue.
+internal_scaling_fp64   Eq. (d) with unrounded operands (used by the tests).
+reference_fp64, folded_fp64     exact-arithmetic references (tests only).
+
+Readings taken where the paper is silent (each applies to both this oracle
+and the HIP path):
+  * The rounding operation of Eq. (a) is round-half-to-even.
+  * Quantization is symmetric and signed: codes lie in [-q, q] with
+    q = 2^(bits-1) - 1 (Eq. (a) with zero point 0, range made signed).
+  * Divisions by a scale are carried out as a float32 multiply by a stored
+    reciprocal for activations, and as a correctly rounded float64 division
+    for weights.
+  * Scales and shifts are computed in float64 and stored in float32.
+  * The activation scale is half the calibrated range over qa, so the
+    calibration extremes map to exactly -qa and +qa after symmetrization.
+  * A constant channel (range 0) gets scale 1; an all-zero weight row gets
+    weight scale 1.
+  * The compensated bias is kept in float32.
+  * Minimum and maximum treat -0 as +0.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+INT32_LIMIT = 2 ** 31
+
+
+class NonFinite(ValueError):
+    """Raised when calibration data or weights contain NaN or infinity."""
+
+
+def qmax(bits: int) -> int:
+    """Largest code of a signed symmetric ``bits``-bit quantizer (Eq. (a))."""
+    if not 2 <= int(bits) <= 8:
+        raise ValueError(f"bits must be in [2, 8], got {bits}")
+    return (1 << (int(bits) - 1)) - 1
+
+
+# --------------------------------------------------------------------------
+# O1: calibration (Sec. 3.2; App. A)
+# --------------------------------------------------------------------------
+def calibrate(batches, a_bits: int):
+    """Static per-channel min-max calibration and symmetrization factors.
+
+    For every input channel k, over all rows of all calibration batches:
+      lo_k, hi_k  = min and max of the channel (fp16 values, exact in fp64);
+      z_k         = (hi_k + lo_k) / 2            -- Sec. 3.2's shift;
+      s_k         = ((hi_k - lo_k) / 2) / qa     -- min-max scale of X - z;
+      inv_s_k     = 1 / s_k.
+    z, s and inv_s are computed in float64 and stored as float32; a channel
+    with hi_k == lo_k (or a scale that underflows float32) gets s_k = 1.
+
+    Returns (minmax, z, s, inv_s): minmax is float32 [2K], the K minima
+    followed by the K maxima (fp16 values, so exact in float32).
+    """
+    qa = qmax(a_bits)
+    lo = hi = None
+    for x in batches:
+        x = np.asarray(x)
+        if x.dtype != np.float16 or x.ndim != 2 or x.shape[0] == 0:
+            raise ValueError("calibration batches must be non-empty fp16 [rows, K]")
+        x64 = x.astype(np.float64) + 0.0  # "+ 0.0" turns -0 into +0
+        if not np.all(np.isfinite(x64)):
+            raise NonFinite("non-finite calibration data")
+        bmin = x64.min(axis=0)
+        bmax = x64.max(axis=0)
+        lo = bmin if lo is None else np.minimum(lo, bmin)
+        hi = bmax if hi is None else np.maximum(hi, bmax)
+    if lo is None:
+        raise ValueError("no calibration batches")
+    z = ((hi + lo) / 2.0).astype(np.float32)
+    half = (hi - lo) / 2.0
+    s = (half / float(qa)).astype(np.float32)
+    s[s == 0] = np.float32(1.0)
+    inv_s = (1.0 / s.astype(np.float64)).astype(np.float32)
+    minmax = np.concatenate([lo, hi]).astype(np.float32)
+    return minmax, z, s, inv_s
+
+
+# --------------------------------------------------------------------------
+# O2: offline weight transform (Eq. (e), (f), (g); Implementation paragraph)
+# --------------------------------------------------------------------------
+def fold_weights(W, b, z, s, w_bits: int):
+    """Fold the activation scale into W, quantize per output channel, and
+    move the symmetrization shift into the bias.
+
+      W_s[n, k]  = W[n, k] * s_k                      Eq. (e) (exact in fp64)
+      sW_n       = max_k |W_s[n, k]| / qw              min-max, per out channel
+      Wq[n, k]   = clip(round(W_s[n, k] / sW_n), -qw, qw)           Eq. (f)
+      b'_n       = sum_k z_k * W[n, k] + b_n   (original W)         Eq. (g)
+
+    The sum for b'_n runs over k in ascending order in float64 (each product
+    is exact), b_n is added last, and the result is stored as float32.
+    ``b`` may be None (no bias).  Returns (Wq int8 [N, K], sW float32 [N],
+    bprime float32 [N]).
+    """
+    qw = qmax(w_bits)
+    W = np.asarray(W)
+    if W.dtype != np.float16 or W.ndim != 2:
+        raise ValueError("W must be fp16 [N, K]")
+    N, K = W.shape
+    W64 = W.astype(np.float64)
+    b64 = np.zeros(N) if b is None else np.asarray(b).astype(np.float64)
+    if not (np.all(np.isfinite(W64)) and np.all(np.isfinite(b64))):
+        raise NonFinite("non-finite weights or bias")
+    s64 = np.asarray(s, dtype=np.float32).astype(np.float64)
+    z64 = np.asarray(z, dtype=np.float32).astype(np.float64)
+    assert s64.shape == (K,) and z64.shape == (K,)
+
+    Ws = W64 * s64[None, :]
+    m = np.abs(Ws).max(axis=1)
+    sW = (m / float(qw)).astype(np.float32)
+    sW[sW == 0] = np.float32(1.0)
+    Wq = np.clip(np.rint(Ws / sW.astype(np.float64)[:, None]), -qw, qw).astype(np.int8)
+
+    acc = np.zeros(N)
+    for k in range(K):
+        acc = acc + z64[k] * W64[:, k]
+    bprime = (acc + b64).astype(np.float32)
+    return Wq, sW, bprime
+
+
+# --------------------------------------------------------------------------
+# O3: runtime activation quantization (Eq. (g))
+# --------------------------------------------------------------------------
+def quantize_act(X, z, inv_s, a_bits: int):
+    """Codes of the symmetrized activations, per input channel:
+
+      t = fp32(X) - z_k        (float32, round to nearest even)
+      u = t * inv_s_k          (float32, round to nearest even)
+      q = clip(round(u), -qa, qa)
+
+    Values outside the calibrated range clip to +-qa.
+    """
+    qa = qmax(a_bits)
+    X = np.asarray(X)
+    if X.dtype != np.float16 or X.ndim != 2:
+        raise ValueError("X must be fp16 [M, K]")
+    z = np.asarray(z, dtype=np.float32)
+    inv_s = np.asarray(inv_s, dtype=np.float32)
+    t = X.astype(np.float32) - z[None, :]
+    u = t * inv_s[None, :]
+    assert u.dtype == np.float32
+    return np.clip(np.rint(u), -qa, qa).astype(np.int8)
+
+
+# --------------------------------------------------------------------------
+# O4: integer GEMM (Eq. (f), right-hand side)
+# --------------------------------------------------------------------------
+def check_acc_range(K: int, a_bits: int, w_bits: int) -> None:
+    """The int32 accumulator cannot overflow iff K * qa * qw < 2^31."""
+    if K * qmax(a_bits) * qmax(w_bits) >= INT32_LIMIT:
+        raise OverflowError("K * qa * qw must be below 2^31")
+
+
+def int_gemm(Xq, Wq):
+    """acc[m, n] = sum_k Xq[m, k] * Wq[n, k], exact, as int32.
+
+    Computed as a float64 matrix product of the integer codes: every partial
+    sum is an integer of magnitude at most K * 127 * 127 < 2^53, so the
+    product is exact whatever order the BLAS sums in.
+    """
+    Xq = np.asarray(Xq)
+    Wq = np.asarray(Wq)
+    assert Xq.ndim == 2 and Wq.ndim == 2 and Xq.shape[1] == Wq.shape[1]
+    K = Xq.shape[1]
+    if K * 127 * 127 >= 2 ** 53:
+        raise OverflowError("K too large for an exact float64 product")
+    acc = Xq.astype(np.float64) @ Wq.astype(np.float64).T
+    return acc.astype(np.int64).astype(np.int32)
+
+
+# --------------------------------------------------------------------------
+# O5: dequantization epilogue (Eq. (g))
+# --------------------------------------------------------------------------
+def epilogue_fp32(acc, sW, bprime):
+    """y = fp32(fp32(fp32(acc) * sW_n) + b'_n), every step float32 RNE."""
+    acc = np.asarray(acc, dtype=np.int32)
+    v = acc.astype(np.float32)
+    p = v * np.asarray(sW, dtype=np.float32)[None, :]
+    y = p + np.asarray(bprime, dtype=np.float32)[None, :]
+    assert y.dtype == np.float32
+    return y
+
+
+def epilogue(acc, sW, bprime):
+    """Y = fp16(y) of :func:`epilogue_fp32` (round to nearest even, +-inf on
+    overflow)."""
+    return epilogue_fp32(acc, sW, bprime).astype(np.float16)
+
+
+def qlinear(Xq, Wq, sW, bprime):
+    """The quantized linear: :func:`int_gemm` then :func:`epilogue`."""
+    return epilogue(int_gemm(Xq, Wq), sW, bprime)
+
+
+# --------------------------------------------------------------------------
+# O6: exact-arithmetic references (tests only)
+# --------------------------------------------------------------------------
+def reference_fp64(X, W, b):
+    """The unquantized linear X W^T + b in float64."""
+    X64 = np.asarray(X).astype(np.float64)
+    W64 = np.asarray(W).astype(np.float64)
+    out = X64 @ W64.T
+    if b is not None:
+        out = out + np.asarray(b).astype(np.float64)[None, :]
+    return out
+
+
+def folded_fp64(X, W, b, z, s):
+    """Eq. (g) with every rounding removed:
+    ((X - z) / s) (W * s)^T + (z W^T + b), in float64."""
+    X64 = np.asarray(X).astype(np.float64)
+    W64 = np.asarray(W).astype(np.float64)
+    z64 = np.asarray(z).astype(np.float64)
+    s64 = np.asarray(s).astype(np.float64)
+    b64 = 0.0 if b is None else np.asarray(b).astype(np.float64)
+    xs = (X64 - z64[None, :]) / s64[None, :]
+    Ws = W64 * s64[None, :]
+    return xs @ Ws.T + (z64[None, :] @ W64.T + b64)
+
+
+def internal_scaling_fp64(Xt, Wt, sX, sWvec):
+    """Eq. (d): Y_ij = s^W_j * sum_k s^X_k * Xt_ik * Wt_kj (Wt given as
+    [N, K], i.e. the paper's W^T), float64, with the scale inside the sum."""
+    Xt = np.asarray(Xt, dtype=np.float64)
+    Wt = np.asarray(Wt, dtype=np.float64)
+    sX = np.asarray(sX, dtype=np.float64)
+    sWvec = np.asarray(sWvec, dtype=np.float64)
+    M, K = Xt.shape
+    N = Wt.shape[0]
+    Y = np.zeros((M, N))
+    for k in range(K):
+        Y += sX[k] * np.outer(Xt[:, k], Wt[:, k])
+    return Y * sWvec[None, :]
+
+
+def pipeline(X, W, b, calib_batches, a_bits: int, w_bits: int):
+    """Calibrate, fold, quantize and run the quantized linear end to end.
+    Returns a dict of every intermediate."""
+    minmax, z, s, inv_s = calibrate(calib_batches, a_bits)
+    Wq, sW, bprime = fold_weights(W, b, z, s, w_bits)
+    Xq = quantize_act(X, z, inv_s, a_bits)
+    check_acc_range(Xq.shape[1], a_bits, w_bits)
+    acc = int_gemm(Xq, Wq)
+    Y = epilogue(acc, sW, bprime)
+    return dict(minmax=minmax, z=z, s=s, inv_s=inv_s, Wq=Wq, sW=sW,
+                bprime=bprime, Xq=Xq, acc=acc, Y=Y)
