@@ -1,0 +1,299 @@
+"""Throughput of OutlierTune's quantized-linear path on one MI355X.
+
+One step = the runtime path of one OPT decoder block's four linears (qkv,
+out, fc1, fc2) on the OPT-13B-shaped W6A6 prefill workload (4096 tokens):
+for each linear, ot_quantize_act (symmetrize + per-channel quantize) then
+ot_qlinear (int8 MFMA GEMM with the fused dequant + bias epilogue).  Inputs
+are seeded synthetic activations with structured outlier channels, already
+resident in HBM; calibration and the weight fold run once, untimed.
+
+Printed: one JSON line.  `value` is int8 TOPS over the whole step (GEMM ops
+2MNK of the four linears divided by the step time, quantization included);
+`roofline` covers the dominant kernel (the prefill GEMM) with its duration
+measured by HIP events around each launch inside the timed region; the
+decode regime (OPT-30B shapes, M in {1, 8, 32, 64}) is reported under
+`decode` in GB/s against HBM; `fp16_baseline` times torch's fp16 linear on
+the same shapes; `cpu_baseline` times the CPU oracle on a bounded sample.
+"""
+from __future__ import annotations
+
+import argparse
+import concurrent.futures as cf
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = ("ot_qlinear int8 TOPS (%MFMA peak) at OPT-13B prefill; GB/s (%HBM) at decode M≤64")
+PEAK_INT8_TOPS = 5000.0    # MI355X dense int8 MFMA, 5.0 POP/s
+PEAK_FP16_TFLOPS = 2500.0  # MI355X dense fp16 MFMA
+PEAK_HBM_GBS = 8000.0      # MI355X HBM3E, 8 TB/s
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=20)
+    p.add_argument("--warmup", type=int, default=5)
+    p.add_argument("--workload", default="opt13b_w6a6")
+    p.add_argument("--decode-workload", default="opt30b_decode_w8a8")
+    p.add_argument("--no-decode", action="store_true", help="skip the decode-regime report")
+    p.add_argument("--no-fp16", action="store_true", help="skip the fp16 torch baseline")
+    p.add_argument("--no-cpu", action="store_true", help="skip the CPU-oracle baseline")
+    p.add_argument("--iters", type=int, default=50, help="iterations for the side measurements")
+    return p.parse_args()
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+# ---------------------------------------------------------------------------
+# Workload preparation (untimed): generate, calibrate, fold
+# ---------------------------------------------------------------------------
+def prepare(wl, rows, torch, ot, synth, pool):
+    """Per layer: GPU-resident X (fp16), z, s, inv_s, Wq, sW, b' and the fp16
+    weight (kept on the host for the fp16 baseline)."""
+    layers = []
+    futs = []
+    for li, lay in enumerate(wl.layers):
+        futs.append((
+            pool.submit(synth.weight, wl, li),
+            pool.submit(synth.bias, wl, li),
+            [pool.submit(synth.activations, wl, li, wl.calib_rows, synth.ROLE_CALIB_X, i)
+             for i in range(wl.calib_batches)],
+            pool.submit(synth.activations, wl, li, rows),
+        ))
+    for li, (fw, fb, fcal, fx) in enumerate(futs):
+        lay = wl.layers[li]
+        batches = (f.result() for f in fcal)
+        _, z, s, inv_s = ot.calibrate(batches, wl.a_bits)
+        W = torch.from_numpy(fw.result()).cuda()
+        b = torch.from_numpy(fb.result()).cuda()
+        Wq, sW, bp = ot.fold_weights(W, b, wl.w_bits, z, s)
+        X = torch.from_numpy(fx.result()).cuda()
+        layers.append(dict(name=lay.name, K=lay.K, N=lay.N, X=X, z=z, s=s, inv_s=inv_s, Wq=Wq,
+                           sW=sW, bp=bp, W16=W, b16=b))
+        log(f"prepared {wl.name}/{lay.name}: K={lay.K} N={lay.N} rows={rows}")
+    return layers
+
+
+def median_ms(torch, fn, iters, warmup=3):
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(iters)]
+    for a, b in ev:
+        a.record()
+        fn()
+        b.record()
+    torch.cuda.synchronize()
+    t = sorted(a.elapsed_time(b) for a, b in ev)
+    return t[len(t) // 2], t[len(t) // 10], t[(9 * len(t)) // 10]
+
+
+# ---------------------------------------------------------------------------
+# Side measurements
+# ---------------------------------------------------------------------------
+def fp16_baseline(torch, layers, M, iters):
+    import torch.nn.functional as F
+    def stack():
+        for L in layers:
+            F.linear(L["X"], L["W16"], L["b16"])
+    med, p10, p90 = median_ms(torch, stack, iters)
+    ops = sum(2.0 * M * L["N"] * L["K"] for L in layers)
+    return dict(ms_per_stack=med, p10_ms=p10, p90_ms=p90, tflops=ops / (med * 1e-3) / 1e12,
+                frac_of_fp16_peak=ops / (med * 1e-3) / 1e12 / PEAK_FP16_TFLOPS)
+
+
+def decode_report(torch, ot, synth, wl, pool, iters, with_fp16):
+    """Weight-streaming regime: the four linears back to back at M tokens.
+    Two copies of the weights alternate so the 256 MB last-level cache cannot
+    serve them."""
+    Mmax = max(wl.decode_M)
+    layers = prepare(wl, Mmax, torch, ot, synth, pool)
+    copies = [layers, [dict(L, Wq=L["Wq"].clone(), sW=L["sW"].clone(), bp=L["bp"].clone())
+                       for L in layers]]
+    out = {}
+    for M in wl.decode_M:
+        xq = [ot.quantize_act(L["X"][:M].contiguous(), wl.a_bits, L["z"], L["inv_s"])
+              for L in layers]
+        ys = [torch.empty((M, L["N"]), dtype=torch.float16, device="cuda") for L in layers]
+        it = [0]
+
+        def stack():
+            c = copies[it[0] & 1]
+            it[0] += 1
+            for i, L in enumerate(c):
+                ot.ot_qlinear(xq[i], L["Wq"], L["sW"], L["bp"], wl.a_bits, wl.w_bits, ys[i])
+        med, p10, p90 = median_ms(torch, stack, iters)
+        nbytes = sum(L["K"] * L["N"] + M * L["K"] + 2 * M * L["N"] + 8 * L["N"] for L in layers)
+        gbs = nbytes / (med * 1e-3) / 1e9
+        rec = dict(us_per_stack=med * 1e3, p10_us=p10 * 1e3, p90_us=p90 * 1e3,
+                   bytes_per_stack=nbytes, GBps=gbs, frac_of_hbm_peak=gbs / PEAK_HBM_GBS,
+                   tokens_per_s=M / (med * 1e-3))
+        if with_fp16:
+            import torch.nn.functional as F
+            w16 = [[L["W16"] for L in layers], [L["W16"].clone() for L in layers]]
+            x16 = [L["X"][:M].contiguous() for L in layers]
+            it16 = [0]
+
+            def stack16():
+                ws = w16[it16[0] & 1]
+                it16[0] += 1
+                for i, L in enumerate(layers):
+                    F.linear(x16[i], ws[i], L["b16"])
+            m16, _, _ = median_ms(torch, stack16, iters)
+            rec["fp16_us_per_stack"] = m16 * 1e3
+            rec["speedup_vs_fp16"] = m16 / med
+            del w16
+        out[str(M)] = rec
+        log(f"decode M={M}: {med * 1e3:.1f} us/stack, {gbs:.0f} GB/s")
+    return out
+
+
+def cpu_baseline(ot_oracle, layers, M, budget_s=10.0):
+    """The oracle's quantize + integer GEMM + epilogue on the first R token
+    rows of every linear, R doubled until the sample takes `budget_s`."""
+    host = [dict(X=L["X"].cpu().numpy(), z=L["z"].cpu().numpy(), inv_s=L["inv_s"].cpu().numpy(),
+                 Wq=L["Wq"].cpu().numpy(), sW=L["sW"].cpu().numpy(), bp=L["bp"].cpu().numpy(),
+                 K=L["K"], N=L["N"]) for L in layers]
+    a_bits = layers[0]["a_bits"]
+    R = 64
+    while True:
+        t0 = time.perf_counter()
+        for h in host:
+            xq = ot_oracle.quantize_act(h["X"][:R], h["z"], h["inv_s"], a_bits)
+            ot_oracle.epilogue(ot_oracle.int_gemm(xq, h["Wq"]), h["sW"], h["bp"])
+        dt = time.perf_counter() - t0
+        if dt >= budget_s or R >= M:
+            break
+        R = min(M, R * 2)
+    ops = sum(2.0 * R * h["N"] * h["K"] for h in host)
+    threads = None
+    try:
+        import threadpoolctl
+        threads = max(i.get("num_threads", 0) for i in threadpoolctl.threadpool_info()) or None
+    except Exception:
+        pass
+    return dict(value=ops / dt / 1e12, unit="TOPS", cores=threads or os.cpu_count(),
+                kind="oracle", seconds=dt,
+                sample=f"first {R} of {M} token rows of each of the 4 linears: quantize_act + "
+                       f"int_gemm (fp64 BLAS) + epilogue; host os.cpu_count()={os.cpu_count()}")
+
+
+# ---------------------------------------------------------------------------
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the quantized linear "
+              "is single-device here and no multi-GPU path is built.", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    from paper_2406_18832_amd import ot, synth
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    ot.lib()
+    wl = synth.WORKLOADS[args.workload]
+    M = wl.M
+    pool = cf.ThreadPoolExecutor(max_workers=min(16, os.cpu_count() or 4))
+    t_setup = time.perf_counter()
+    layers = prepare(wl, M, torch, ot, synth, pool)
+    for L in layers:
+        L["a_bits"] = wl.a_bits
+        L["Xq"] = torch.empty((M, L["K"]), dtype=torch.int8, device="cuda")
+        L["Y"] = torch.empty((M, L["N"]), dtype=torch.float16, device="cuda")
+    log(f"setup {time.perf_counter() - t_setup:.1f}s")
+
+    nl = len(layers)
+    ev_q = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+             for _ in range(nl)] for _ in range(args.steps)]
+
+    def step(events=None):
+        for i, L in enumerate(layers):
+            ot.ot_quantize_act(L["X"], wl.a_bits, L["z"], L["inv_s"], L["Xq"])
+            if events is not None:
+                events[i][0].record()
+            ot.ot_qlinear(L["Xq"], L["Wq"], L["sW"], L["bp"], wl.a_bits, wl.w_bits, L["Y"])
+            if events is not None:
+                events[i][1].record()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    start.record()
+    for k in range(args.steps):
+        step(ev_q[k])
+    end.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_step = start.elapsed_time(end) / args.steps
+    ops_step = sum(2.0 * M * L["N"] * L["K"] for L in layers)
+    tops = ops_step / (ms_step * 1e-3) / 1e12
+    per_layer_ms = [float(np.mean([ev_q[k][i][0].elapsed_time(ev_q[k][i][1])
+                                   for k in range(args.steps)])) for i in range(nl)]
+    gemm_ms = sum(per_layer_ms)
+    gemm_tops = ops_step / (gemm_ms * 1e-3) / 1e12
+    log(f"step {ms_step:.3f} ms ({tops:.0f} TOPS); qlinear {gemm_ms:.3f} ms ({gemm_tops:.0f} TOPS); "
+        f"wall {wall:.2f}s")
+
+    result = {
+        "metric": METRIC,
+        "value": round(tops, 2),
+        "unit": "TOPS",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int8",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "tokens": M, "a_bits": wl.a_bits, "w_bits": wl.w_bits,
+                   "layers": {L["name"]: [L["K"], L["N"]] for L in layers},
+                   "step": "4 x (ot_quantize_act + ot_qlinear)"},
+        "roofline": {"bound": "mfma", "kernel": "qgemm_prefill",
+                     "achieved": round(gemm_tops, 2), "peak": PEAK_INT8_TOPS, "unit": "TOP/s",
+                     "frac": round(gemm_tops / PEAK_INT8_TOPS, 4), "traffic": None,
+                     "ops_per_launch": {L["name"]: 2 * M * L["N"] * L["K"] for L in layers},
+                     "ms_per_launch": {L["name"]: round(t, 4) for L, t in zip(layers, per_layer_ms)}},
+        "qlinear_tops": round(gemm_tops, 2),
+        "quantize_act_ms_per_step": round(ms_step - gemm_ms, 4),
+        "tokens_per_s": round(M / (ms_step * 1e-3), 1),
+    }
+    if not args.no_fp16:
+        fb = fp16_baseline(torch, layers, M, args.iters)
+        fb["speedup_of_step"] = fb["ms_per_stack"] / ms_step
+        fb["weight_bytes_ratio"] = (sum(2 * L["K"] * L["N"] + 2 * L["N"] for L in layers) /
+                                    sum(L["K"] * L["N"] + 8 * L["N"] for L in layers))
+        result["fp16_baseline"] = fb
+        log(f"fp16 linear stack {fb['ms_per_stack']:.3f} ms ({fb['tflops']:.0f} TFLOPs)")
+    if not args.no_cpu:
+        from oracle import ot_oracle
+        result["cpu_baseline"] = cpu_baseline(ot_oracle, layers, M)
+        log(f"cpu oracle {result['cpu_baseline']['value']:.3f} TOPS")
+    for L in layers:
+        del L["W16"]
+    if not args.no_decode:
+        dwl = synth.WORKLOADS[args.decode_workload]
+        layers.clear()
+        torch.cuda.empty_cache()
+        result["decode"] = {"workload": dwl.name, "bound": "hbm", "peak_GBps": PEAK_HBM_GBS,
+                            "by_M": decode_report(torch, ot, synth, dwl, pool, args.iters,
+                                                  not args.no_fp16)}
+    pool.shutdown()
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

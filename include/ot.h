@@ -1,0 +1,162 @@
+/*
+ * ot.h -- C ABI of libot, OutlierTune's per-channel-quantized linear layer
+ * for AMD Instinct MI355X (gfx950).
+ *
+ * The library implements the inference path of OutlierTune (Wang et al.,
+ * 2024): static per-channel calibration of the activations with a
+ * symmetrization shift (Sec. 3.2, App. A), the offline fold of the
+ * activation scale into the weights and of the shift into the bias
+ * (Sec. 3.1 Eq. (e), Eq. (f), Sec. 3.2 Eq. (g)), runtime per-channel
+ * quantization of the activations (Eq. (g)), and the integer GEMM with a
+ * dequantizing epilogue (Eq. (f) right-hand side, Eq. (g)).
+ *
+ * Conventions shared by every entry point
+ *  - Tensors are dense and row-major (leading dimension = inner size).
+ *    X is [M x K] (tokens x input channels); the weight W is [N x K], the
+ *    layout of a PyTorch nn.Linear weight, so the paper's W^T is its
+ *    transpose.
+ *  - Every tensor pointer is a DEVICE pointer owned by the caller.  The
+ *    library never allocates, frees or retains caller memory and keeps no
+ *    global state; calls on different streams are independent.
+ *  - fp16 tensors are passed as uint16_t IEEE binary16 bit patterns.
+ *  - bits is in [2, 8]; the quantizer is symmetric and signed with largest
+ *    code q(bits) = 2^(bits-1) - 1 (127 for 8 bits, 31 for 6 bits).  Codes
+ *    are stored in int8 whatever the bit-width.  Rounding is round half to
+ *    even throughout.
+ *  - stream is a hipStream_t passed as void* (NULL = the default stream).
+ *  - Every argument check happens on the host before any launch: on an
+ *    error status no kernel runs and no output is written, except where an
+ *    entry point says otherwise.  A fault inside an asynchronous kernel
+ *    surfaces as OT_EHIP from a later synchronous call or from the caller's
+ *    own stream synchronization.
+ */
+#ifndef OT_H_
+#define OT_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum ot_status {
+  OT_OK = 0,
+  OT_EINVAL = 1,     /* null pointer, bits outside [2, 8], negative size     */
+  OT_ESHAPE = 2,     /* K not a multiple of 16, zero-sized where disallowed  */
+  OT_ERANGE = 3,     /* K * qa * qw >= 2^31: the int32 accumulator could wrap */
+  OT_ENONFINITE = 4, /* NaN or infinity in calibration data or weights       */
+  OT_EHIP = 5        /* a HIP runtime call failed                            */
+} ot_status;
+
+/* Static, human-readable description of a status code. */
+const char *ot_strerror(int status);
+
+/* Version of this ABI (bumped on any incompatible change). */
+int ot_abi_version(void);
+
+/*
+ * ot_calibrate -- static min-max calibration and symmetrization factors.
+ * Sec. 3.2 (z = (max + min) / 2 per channel, X_hat = X - z) and App. A
+ * (min-max calibration of the activations, done offline).
+ *
+ *   x       [rows x K] fp16 calibration activations (device).
+ *   rows    >= 1.   K >= 1.
+ *   a_bits  activation bit-width, in [2, 8]; qa = 2^(a_bits-1) - 1.
+ *   first   nonzero: reset the running state before folding this batch in;
+ *           zero: accumulate into the state left by earlier calls.
+ *   minmax  [2K] fp32 running state (device): the K per-channel minima then
+ *           the K maxima.  -0 is recorded as +0.
+ *   z, s, inv_s  [K] fp32 outputs (device), rewritten from the running state
+ *           on every call, so they are final after the last batch:
+ *             z_k     = fp32((hi_k + lo_k) / 2)
+ *             s_k     = fp32(((hi_k - lo_k) / 2) / qa), 1 if that is 0
+ *             inv_s_k = fp32(1 / s_k)
+ *           (fp64 arithmetic, each result rounded once to fp32).
+ *
+ * Synchronous: waits for the stream.  Returns OT_ENONFINITE if the running
+ * state holds a NaN or an infinity (then z, s, inv_s are not written; the
+ * state stays poisoned until a call with first != 0).
+ */
+ot_status ot_calibrate(const uint16_t *x, int64_t rows, int64_t K, int a_bits,
+                       int first, float *minmax, float *z, float *s,
+                       float *inv_s, void *stream);
+
+/*
+ * ot_fold_weights -- the offline weight and bias transform.
+ * Sec. 3.1 Eq. (e) (W_s = W scaled by s along the input channels), Eq. (f)
+ * (per-output-channel quantization of W_s), Sec. 3.2 Eq. (g) (the shift z
+ * moves into the bias, b' = z W^T + b), Implementation paragraph (the
+ * weight quantization is done once, offline).
+ *
+ *   W       [N x K] fp16 weight (device).      b [N] fp16 bias or NULL.
+ *   w_bits  weight bit-width in [2, 8]; qw = 2^(w_bits-1) - 1.
+ *   z, s    [K] fp32 from ot_calibrate (device).
+ *   Wq      [N x K] int8 output: clip(rne(W[n,k] s_k / sW_n), -qw, qw).
+ *   sW      [N] fp32 output: fp32(max_k |W[n,k] s_k| / qw), 1 for a zero row.
+ *   bprime  [N] fp32 output: fp32(sum_k z_k W[n,k] + b_n), summed in fp64
+ *           (the summation order is unspecified, so it can differ from a
+ *           sequential sum in the last fp32 place).
+ *   The products W[n,k] s_k are exact in fp64, the division by sW_n is a
+ *   correctly rounded fp64 division.
+ *
+ * Synchronous.  OT_ENONFINITE if W or b holds a NaN or an infinity; then
+ * the contents of Wq, sW and bprime are unspecified.
+ */
+ot_status ot_fold_weights(const uint16_t *W, const uint16_t *b, int64_t N,
+                          int64_t K, int w_bits, const float *z, const float *s,
+                          int8_t *Wq, float *sW, float *bprime, void *stream);
+
+/*
+ * ot_quantize_act -- runtime symmetrize + per-channel quantize, Eq. (g):
+ *   Xq[m,k] = clip(rne(fp32(fp32(x[m,k]) - z_k) * inv_s_k), -qa, qa)
+ * with both fp32 operations rounded to nearest even (no fused multiply-add).
+ * Values outside the calibrated range clip; NaN input gives unspecified
+ * codes.
+ *
+ *   x      [M x K] fp16 (device).  M >= 0 (0 is a no-op), K >= 16, K % 16 == 0.
+ *   z, inv_s  [K] fp32 (device).    Xq [M x K] int8 output (device).
+ *
+ * Asynchronous on stream.
+ */
+ot_status ot_quantize_act(const uint16_t *x, int64_t M, int64_t K, int a_bits,
+                          const float *z, const float *inv_s, int8_t *Xq,
+                          void *stream);
+
+/*
+ * ot_qlinear -- the quantized linear: integer GEMM (Eq. (f) right-hand side)
+ * with the fused dequantizing epilogue of Eq. (g):
+ *   acc[m,n] = sum_k Xq[m,k] Wq[n,k]                       (exact int32)
+ *   Y[m,n]   = fp16(fp32(fp32(acc[m,n]) * sW_n) + bprime_n)
+ * every conversion and operation rounded to nearest even, no fused
+ * multiply-add.  Prefill shapes run on the int8 matrix cores; M <= 64 runs
+ * a weight-streaming decode kernel.  Both give bit-identical results.
+ *
+ *   Xq [M x K] int8, Wq [N x K] int8, sW [N] fp32, bprime [N] fp32 (device).
+ *   M >= 0 (0 is a no-op), N >= 1, K >= 16 with K % 16 == 0.
+ *   a_bits, w_bits  the bit-widths the codes were made with; they bound the
+ *           codes (|Xq| <= qa, |Wq| <= qw) and so the accumulator:
+ *           OT_ERANGE if K * qa * qw >= 2^31.  Codes outside those bounds
+ *           give unspecified results.
+ *   Y      [M x N] fp16 output (device).
+ *   acc_out  NULL, or [M x N] int32 (device) that also receives acc (for
+ *           testing; costs extra memory traffic).
+ *   workspace  NULL, or at least ot_qlinear_workspace_size(M, N, K) bytes of
+ *           device memory the call may use as scratch; with NULL the call
+ *           uses no scratch memory.  Results do not depend on it.
+ *
+ * Asynchronous on stream; no synchronization, no allocation.
+ */
+ot_status ot_qlinear(const int8_t *Xq, const int8_t *Wq, const float *sW,
+                     const float *bprime, int64_t M, int64_t N, int64_t K,
+                     int a_bits, int w_bits, uint16_t *Y, int32_t *acc_out,
+                     void *workspace, void *stream);
+
+/* Bytes of optional scratch ot_qlinear can use for these sizes (0 if none). */
+size_t ot_qlinear_workspace_size(int64_t M, int64_t N, int64_t K);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* OT_H_ */

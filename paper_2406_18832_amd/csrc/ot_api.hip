@@ -1,0 +1,127 @@
+// C ABI of libot (declared in include/ot.h): argument checks on the host,
+// then kernel launches on the caller's stream.  Nothing here allocates
+// device memory or keeps state between calls.
+#include <math.h>
+#include <string.h>
+
+#include <vector>
+
+#include "ot_common.h"
+
+namespace {
+
+// Largest K the kernels' 32-bit in-tile offsets cover (a 256-row tile of
+// K-byte rows must stay below 2^31 bytes).
+constexpr int64_t kMaxK = int64_t(1) << 22;
+constexpr int64_t kMaxRows = (int64_t(1) << 31) - 1;
+
+bool bits_ok(int bits) { return bits >= 2 && bits <= 8; }
+int qmax(int bits) { return (1 << (bits - 1)) - 1; }
+bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+ot_status hip_status(hipError_t e) { return e == hipSuccess ? OT_OK : OT_EHIP; }
+
+bool all_finite(const std::vector<float> &v) {
+  for (float f : v)
+    if (!isfinite(f)) return false;
+  return true;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *ot_strerror(int status) {
+  switch (status) {
+    case OT_OK: return "ok";
+    case OT_EINVAL: return "invalid argument (null or misaligned pointer, bits outside [2, 8], negative size)";
+    case OT_ESHAPE: return "unsupported shape (K must be a positive multiple of 16 within limits; sizes must be nonzero where required)";
+    case OT_ERANGE: return "K * qa * qw >= 2^31: the int32 accumulator could overflow";
+    case OT_ENONFINITE: return "non-finite value (NaN or infinity) in calibration data or weights";
+    case OT_EHIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+int ot_abi_version(void) { return 1; }
+
+ot_status ot_calibrate(const uint16_t *x, int64_t rows, int64_t K, int a_bits, int first,
+                       float *minmax, float *z, float *s, float *inv_s, void *stream) {
+  if (!x || !minmax || !z || !s || !inv_s) return OT_EINVAL;
+  if (!bits_ok(a_bits) || rows < 0 || K < 0) return OT_EINVAL;
+  if (rows == 0 || K == 0 || rows > kMaxRows || K > kMaxRows) return OT_ESHAPE;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  ot_status rc;
+  if (first && (rc = hip_status(ot::launch_calib_reset(minmax, K, st))) != OT_OK) return rc;
+  if ((rc = hip_status(ot::launch_calib_minmax(x, rows, K, minmax, st))) != OT_OK) return rc;
+  std::vector<float> state((size_t)(2 * K));
+  if ((rc = hip_status(hipMemcpyAsync(state.data(), minmax, sizeof(float) * 2 * K,
+                                      hipMemcpyDeviceToHost, st))) != OT_OK)
+    return rc;
+  if ((rc = hip_status(hipStreamSynchronize(st))) != OT_OK) return rc;
+  if (!all_finite(state)) return OT_ENONFINITE;
+  if ((rc = hip_status(ot::launch_calib_finalize(minmax, K, qmax(a_bits), z, s, inv_s, st))) !=
+      OT_OK)
+    return rc;
+  return hip_status(hipStreamSynchronize(st));
+}
+
+ot_status ot_fold_weights(const uint16_t *W, const uint16_t *b, int64_t N, int64_t K, int w_bits,
+                          const float *z, const float *s, int8_t *Wq, float *sW, float *bprime,
+                          void *stream) {
+  if (!W || !z || !s || !Wq || !sW || !bprime) return OT_EINVAL;
+  if (!bits_ok(w_bits) || N < 0 || K < 0) return OT_EINVAL;
+  if (N == 0 || K == 0 || N > kMaxRows || K > kMaxRows) return OT_ESHAPE;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  ot_status rc;
+  if ((rc = hip_status(ot::launch_fold(W, b, N, K, qmax(w_bits), z, s, Wq, sW, bprime, st))) !=
+      OT_OK)
+    return rc;
+  std::vector<float> scale((size_t)N), bias((size_t)N);
+  if ((rc = hip_status(hipMemcpyAsync(scale.data(), sW, sizeof(float) * N, hipMemcpyDeviceToHost,
+                                      st))) != OT_OK ||
+      (rc = hip_status(hipMemcpyAsync(bias.data(), bprime, sizeof(float) * N,
+                                      hipMemcpyDeviceToHost, st))) != OT_OK)
+    return rc;
+  if ((rc = hip_status(hipStreamSynchronize(st))) != OT_OK) return rc;
+  if (!all_finite(scale) || !all_finite(bias)) return OT_ENONFINITE;
+  return OT_OK;
+}
+
+ot_status ot_quantize_act(const uint16_t *x, int64_t M, int64_t K, int a_bits, const float *z,
+                          const float *inv_s, int8_t *Xq, void *stream) {
+  if (!bits_ok(a_bits) || M < 0 || K < 0) return OT_EINVAL;
+  if (K < 16 || K % 16 != 0 || K > kMaxK || M > kMaxRows) return OT_ESHAPE;
+  if (M == 0) return OT_OK;
+  if (!x || !z || !inv_s || !Xq) return OT_EINVAL;
+  if (!aligned16(x) || !aligned16(z) || !aligned16(inv_s) || !aligned16(Xq)) return OT_EINVAL;
+  return hip_status(ot::launch_quantize_act(x, M, K, qmax(a_bits), z, inv_s, Xq,
+                                            static_cast<hipStream_t>(stream)));
+}
+
+ot_status ot_qlinear(const int8_t *Xq, const int8_t *Wq, const float *sW, const float *bprime,
+                     int64_t M, int64_t N, int64_t K, int a_bits, int w_bits, uint16_t *Y,
+                     int32_t *acc_out, void *workspace, void *stream) {
+  (void)workspace;
+  if (!bits_ok(a_bits) || !bits_ok(w_bits) || M < 0 || N < 0 || K < 0) return OT_EINVAL;
+  if (N == 0 || K < 16 || K % 16 != 0 || K > kMaxK || M > kMaxRows || N > kMaxRows)
+    return OT_ESHAPE;
+  if ((M + 255) / 256 * ((N + 255) / 256) > kMaxRows) return OT_ESHAPE;
+  if (K * qmax(a_bits) * qmax(w_bits) >= (int64_t(1) << 31)) return OT_ERANGE;
+  if (M == 0) return OT_OK;
+  if (!Xq || !Wq || !sW || !bprime || !Y) return OT_EINVAL;
+  if (!aligned16(Xq) || !aligned16(Wq) || !aligned16(sW) || !aligned16(bprime) || !aligned16(Y) ||
+      (acc_out && !aligned16(acc_out)))
+    return OT_EINVAL;
+  return hip_status(ot::launch_qgemm(Xq, Wq, sW, bprime, M, N, K, Y, acc_out,
+                                     static_cast<hipStream_t>(stream)));
+}
+
+size_t ot_qlinear_workspace_size(int64_t M, int64_t N, int64_t K) {
+  (void)M;
+  (void)N;
+  (void)K;
+  return 0;
+}
+
+}  // extern "C"

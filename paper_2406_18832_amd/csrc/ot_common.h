@@ -1,0 +1,53 @@
+// Internal declarations shared by libot's translation units (not installed).
+//
+// Every translation unit is compiled for gfx950 only, with floating-point
+// contraction off: the method's roundings are specified step by step, and
+// a fused multiply-add would skip one of them.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/ot.h"
+
+namespace ot {
+
+typedef int v4i __attribute__((ext_vector_type(4)));
+typedef int v16i __attribute__((ext_vector_type(16)));
+
+// Word 3 of a raw (untyped) buffer resource on gfx9-family GPUs.
+constexpr uint32_t kRsrcWord3 = 0x00020000u;
+// A byte offset no buffer here reaches: a load from it returns zeros.
+constexpr uint32_t kOobOffset = 0x80000000u;
+
+__device__ inline __amdgpu_buffer_rsrc_t make_rsrc(const void *base, uint32_t nbytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), 0, (int)nbytes,
+                                           (int)kRsrcWord3);
+}
+
+__device__ inline float half_bits_to_float(uint16_t h) {
+  return (float)__builtin_bit_cast(_Float16, h);
+}
+
+// fp32 -> fp16, round to nearest even, +-inf on overflow.
+__device__ inline uint16_t float_to_half_bits(float f) {
+  return __builtin_bit_cast(uint16_t, (_Float16)f);
+}
+
+// Launchers: each validates nothing (the C ABI layer does) and returns the
+// launch status.
+hipError_t launch_calib_reset(float *minmax, int64_t K, hipStream_t st);
+hipError_t launch_calib_minmax(const uint16_t *x, int64_t rows, int64_t K, float *minmax,
+                               hipStream_t st);
+hipError_t launch_calib_finalize(const float *minmax, int64_t K, int qa, float *z, float *s,
+                                 float *inv_s, hipStream_t st);
+hipError_t launch_fold(const uint16_t *W, const uint16_t *b, int64_t N, int64_t K, int qw,
+                       const float *z, const float *s, int8_t *Wq, float *sW, float *bprime,
+                       hipStream_t st);
+hipError_t launch_quantize_act(const uint16_t *x, int64_t M, int64_t K, int qa, const float *z,
+                               const float *inv_s, int8_t *Xq, hipStream_t st);
+hipError_t launch_qgemm(const int8_t *Xq, const int8_t *Wq, const float *sW, const float *bprime,
+                        int64_t M, int64_t N, int64_t K, uint16_t *Y, int32_t *acc_out,
+                        hipStream_t st);
+
+}  // namespace ot

@@ -1,0 +1,76 @@
+// Runtime symmetrize + per-channel quantize (OutlierTune Sec. 3.2, Eq. (g):
+// the codes round((X - z) / s^X) with static per-channel z and s).
+//
+//   Xq[m, k] = clip(rne(fp32(fp32(x[m, k]) - z_k) * inv_s_k), -qa, qa)
+//
+// HBM-bound streaming kernel: 2 bytes in, 1 byte out per element.  A wave
+// covers 64 x 16 = 1024 consecutive channels of one row (32-byte loads and
+// 16-byte stores per lane, fully coalesced) and keeps those channels' z and
+// inv_s in registers while it walks down kRowsPerWave rows.
+#include "ot_common.h"
+
+namespace ot {
+namespace detail {
+
+constexpr int kWavesPerBlock = 4;
+constexpr int kRowsPerWave = 8;
+
+__device__ inline uint32_t pack4(int a, int b, int c, int d) {
+  return (uint32_t)(a & 0xff) | ((uint32_t)(b & 0xff) << 8) | ((uint32_t)(c & 0xff) << 16) |
+         ((uint32_t)(d & 0xff) << 24);
+}
+
+__global__ __launch_bounds__(64 * kWavesPerBlock) void quantize_act_kernel(
+    const uint16_t *__restrict__ x, int64_t M, int64_t K, float qa, const float *__restrict__ z,
+    const float *__restrict__ inv_s, int8_t *__restrict__ Xq) {
+  const int64_t chunk = (int64_t)blockIdx.x * 64 + threadIdx.x;  // 16-channel chunk
+  const int64_t k0 = chunk * 16;
+  if (k0 >= K) return;
+  float zr[16], ir[16];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const float4 zz = reinterpret_cast<const float4 *>(z + k0)[i];
+    const float4 ii = reinterpret_cast<const float4 *>(inv_s + k0)[i];
+    zr[4 * i + 0] = zz.x; zr[4 * i + 1] = zz.y; zr[4 * i + 2] = zz.z; zr[4 * i + 3] = zz.w;
+    ir[4 * i + 0] = ii.x; ir[4 * i + 1] = ii.y; ir[4 * i + 2] = ii.z; ir[4 * i + 3] = ii.w;
+  }
+  const int64_t row_step = (int64_t)gridDim.y * kWavesPerBlock;
+  for (int64_t r = (int64_t)blockIdx.y * kWavesPerBlock + threadIdx.y; r < M;
+       r += row_step) {
+    const uint4 *src = reinterpret_cast<const uint4 *>(x + r * K + k0);
+    const uint4 lo = src[0], hi = src[1];
+    const uint32_t words[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+    int q[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const uint16_t h = (uint16_t)(words[i >> 1] >> (16 * (i & 1)));
+      const float t = half_bits_to_float(h) - zr[i];  // fp32, RNE
+      const float u = t * ir[i];                      // fp32, RNE
+      q[i] = (int)rintf(fminf(fmaxf(u, -qa), qa));
+    }
+    uint4 out;
+    out.x = pack4(q[0], q[1], q[2], q[3]);
+    out.y = pack4(q[4], q[5], q[6], q[7]);
+    out.z = pack4(q[8], q[9], q[10], q[11]);
+    out.w = pack4(q[12], q[13], q[14], q[15]);
+    *reinterpret_cast<uint4 *>(Xq + r * K + k0) = out;
+  }
+}
+
+}  // namespace detail
+
+using namespace detail;
+
+hipError_t launch_quantize_act(const uint16_t *x, int64_t M, int64_t K, int qa, const float *z,
+                               const float *inv_s, int8_t *Xq, hipStream_t st) {
+  const int64_t chunks = K / 16;
+  const unsigned gx = (unsigned)((chunks + 63) / 64);
+  int64_t gy = (M + (int64_t)kWavesPerBlock * kRowsPerWave - 1) /
+               ((int64_t)kWavesPerBlock * kRowsPerWave);
+  if (gy > 65535) gy = 65535;
+  dim3 block(64, kWavesPerBlock);
+  quantize_act_kernel<<<dim3(gx, (unsigned)gy), block, 0, st>>>(x, M, K, (float)qa, z, inv_s, Xq);
+  return hipGetLastError();
+}
+
+}  // namespace ot

@@ -1,0 +1,203 @@
+"""Thin Python binding of libot's C ABI (include/ot.h).
+
+Argument marshalling only: torch tensors in, device pointers and the current
+HIP stream out to the library; every computation runs in libot's kernels.
+The names match the C entry points.  Outputs are caller-allocated, as in C.
+
+The library is loaded on first use.  If ``libot.so`` has not been built the
+first call raises: there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libot.so")
+HEADER = os.path.join(os.path.dirname(HERE), "include", "ot.h")
+
+OT_OK, OT_EINVAL, OT_ESHAPE, OT_ERANGE, OT_ENONFINITE, OT_EHIP = range(6)
+
+_lib = None
+
+
+class OTError(RuntimeError):
+    """A nonzero ot_status from libot."""
+
+    def __init__(self, code: int, where: str):
+        self.code = int(code)
+        super().__init__(f"{where}: {ot_strerror(code)} (status {code})")
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded libot (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with __graft_entry__.build()")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, i64, c_int = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int
+        L.ot_strerror.restype = ctypes.c_char_p
+        L.ot_strerror.argtypes = [c_int]
+        L.ot_abi_version.restype = c_int
+        L.ot_abi_version.argtypes = []
+        L.ot_calibrate.restype = c_int
+        L.ot_calibrate.argtypes = [vp, i64, i64, c_int, c_int, vp, vp, vp, vp, vp]
+        L.ot_fold_weights.restype = c_int
+        L.ot_fold_weights.argtypes = [vp, vp, i64, i64, c_int, vp, vp, vp, vp, vp, vp]
+        L.ot_quantize_act.restype = c_int
+        L.ot_quantize_act.argtypes = [vp, i64, i64, c_int, vp, vp, vp, vp]
+        L.ot_qlinear.restype = c_int
+        L.ot_qlinear.argtypes = [vp, vp, vp, vp, i64, i64, i64, c_int, c_int, vp, vp, vp, vp]
+        L.ot_qlinear_workspace_size.restype = ctypes.c_size_t
+        L.ot_qlinear_workspace_size.argtypes = [i64, i64, i64]
+        _lib = L
+    return _lib
+
+
+def declared_symbols() -> list:
+    """Entry points declared in include/ot.h."""
+    with open(HEADER) as f:
+        text = f.read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?[\w\s\*]+?\b(ot_\w+)\s*\(", text, re.M)))
+
+
+def ot_strerror(code: int) -> str:
+    return lib().ot_strerror(int(code)).decode()
+
+
+def ot_abi_version() -> int:
+    return int(lib().ot_abi_version())
+
+
+def _check(rc: int, where: str) -> None:
+    if rc != OT_OK:
+        raise OTError(rc, where)
+
+
+def _dev(t, dtype, name, shape=None):
+    if t is None:
+        return None
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be on the GPU")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+    return t.data_ptr()
+
+
+def _stream(stream):
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, torch.cuda.Stream):
+        return stream.cuda_stream
+    return int(stream)
+
+
+def ot_calibrate(x, a_bits, first, minmax, z, s, inv_s, stream=None):
+    """Folds the calibration batch x [rows, K] fp16 into minmax [2K] and
+    rewrites z, s, inv_s [K] (fp32).  Synchronous."""
+    rows, K = x.shape
+    rc = lib().ot_calibrate(_dev(x, torch.float16, "x"), rows, K, int(a_bits), int(bool(first)),
+                            _dev(minmax, torch.float32, "minmax", (2 * K,)),
+                            _dev(z, torch.float32, "z", (K,)), _dev(s, torch.float32, "s", (K,)),
+                            _dev(inv_s, torch.float32, "inv_s", (K,)), _stream(stream))
+    _check(rc, "ot_calibrate")
+
+
+def ot_fold_weights(W, b, w_bits, z, s, Wq, sW, bprime, stream=None):
+    """W [N, K] fp16, b [N] fp16 or None -> Wq [N, K] int8, sW, bprime [N]
+    fp32.  Synchronous."""
+    N, K = W.shape
+    rc = lib().ot_fold_weights(_dev(W, torch.float16, "W"), _dev(b, torch.float16, "b", (N,)),
+                               N, K, int(w_bits), _dev(z, torch.float32, "z", (K,)),
+                               _dev(s, torch.float32, "s", (K,)),
+                               _dev(Wq, torch.int8, "Wq", (N, K)),
+                               _dev(sW, torch.float32, "sW", (N,)),
+                               _dev(bprime, torch.float32, "bprime", (N,)), _stream(stream))
+    _check(rc, "ot_fold_weights")
+
+
+def ot_quantize_act(x, a_bits, z, inv_s, Xq, stream=None):
+    """x [M, K] fp16 -> Xq [M, K] int8.  Asynchronous."""
+    M, K = x.shape
+    rc = lib().ot_quantize_act(_dev(x, torch.float16, "x"), M, K, int(a_bits),
+                               _dev(z, torch.float32, "z", (K,)),
+                               _dev(inv_s, torch.float32, "inv_s", (K,)),
+                               _dev(Xq, torch.int8, "Xq", (M, K)), _stream(stream))
+    _check(rc, "ot_quantize_act")
+
+
+def ot_qlinear(Xq, Wq, sW, bprime, a_bits, w_bits, Y, acc_out=None, workspace=None, stream=None):
+    """Xq [M, K] int8, Wq [N, K] int8 -> Y [M, N] fp16 (and acc_out [M, N]
+    int32 if given).  Asynchronous."""
+    M, K = Xq.shape
+    N = Wq.shape[0]
+    if Wq.shape[1] != K:
+        raise ValueError("Xq and Wq disagree on K")
+    ws = None if workspace is None else _dev(workspace, torch.uint8, "workspace")
+    rc = lib().ot_qlinear(_dev(Xq, torch.int8, "Xq"), _dev(Wq, torch.int8, "Wq"),
+                          _dev(sW, torch.float32, "sW", (N,)),
+                          _dev(bprime, torch.float32, "bprime", (N,)), M, N, K, int(a_bits),
+                          int(w_bits), _dev(Y, torch.float16, "Y", (M, N)),
+                          _dev(acc_out, torch.int32, "acc_out", (M, N)), ws, _stream(stream))
+    _check(rc, "ot_qlinear")
+
+
+def ot_qlinear_workspace_size(M: int, N: int, K: int) -> int:
+    return int(lib().ot_qlinear_workspace_size(M, N, K))
+
+
+# ---------------------------------------------------------------------------
+# Conveniences that allocate outputs with torch and call the entry points.
+# ---------------------------------------------------------------------------
+def calibrate(batches, a_bits, device="cuda"):
+    """Runs ot_calibrate over an iterable of fp16 [rows, K] batches (host
+    numpy or device tensors).  Returns (minmax, z, s, inv_s) on the GPU."""
+    minmax = z = s = inv_s = None
+    first = True
+    for x in batches:
+        if not isinstance(x, torch.Tensor):
+            x = torch.from_numpy(x)
+        x = x.to(device)
+        K = x.shape[1]
+        if minmax is None:
+            minmax = torch.empty(2 * K, dtype=torch.float32, device=device)
+            z, s, inv_s = (torch.empty(K, dtype=torch.float32, device=device) for _ in range(3))
+        ot_calibrate(x, a_bits, first, minmax, z, s, inv_s)
+        first = False
+    if minmax is None:
+        raise ValueError("no calibration batches")
+    return minmax, z, s, inv_s
+
+
+def fold_weights(W, b, w_bits, z, s):
+    """Allocating wrapper of ot_fold_weights; returns (Wq, sW, bprime)."""
+    N, K = W.shape
+    Wq = torch.empty((N, K), dtype=torch.int8, device=W.device)
+    sW = torch.empty(N, dtype=torch.float32, device=W.device)
+    bprime = torch.empty(N, dtype=torch.float32, device=W.device)
+    ot_fold_weights(W, b, w_bits, z, s, Wq, sW, bprime)
+    return Wq, sW, bprime
+
+
+def quantize_act(x, a_bits, z, inv_s):
+    Xq = torch.empty(x.shape, dtype=torch.int8, device=x.device)
+    ot_quantize_act(x, a_bits, z, inv_s, Xq)
+    return Xq
+
+
+def qlinear(Xq, Wq, sW, bprime, a_bits, w_bits, want_acc=False):
+    M, N = Xq.shape[0], Wq.shape[0]
+    Y = torch.empty((M, N), dtype=torch.float16, device=Xq.device)
+    acc = torch.empty((M, N), dtype=torch.int32, device=Xq.device) if want_acc else None
+    ot_qlinear(Xq, Wq, sW, bprime, a_bits, w_bits, Y, acc)
+    return (Y, acc) if want_acc else Y

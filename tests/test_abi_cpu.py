@@ -1,0 +1,93 @@
+"""Host-side checks of libot that need no GPU: the library loads, exports
+every entry point include/ot.h declares, and rejects bad arguments before
+any HIP call (so these calls are safe without a device)."""
+import ctypes
+import os
+import subprocess
+
+import pytest
+
+from paper_2406_18832_amd import ot
+
+LIB = ot.LIB_PATH
+
+
+def test_library_is_built():
+    assert os.path.exists(LIB), "run __graft_entry__.build() first"
+
+
+def test_exports_every_declared_symbol():
+    declared = ot.declared_symbols()
+    assert {"ot_calibrate", "ot_fold_weights", "ot_quantize_act", "ot_qlinear"} <= set(declared)
+    L = ctypes.CDLL(LIB)
+    for name in declared:
+        assert hasattr(L, name), f"{name} declared in ot.h but not exported"
+    out = subprocess.run(["nm", "-D", "--defined-only", LIB], capture_output=True, text=True)
+    exported = {line.split()[-1] for line in out.stdout.splitlines() if " T ot_" in line}
+    assert exported == set(declared)
+
+
+def test_strerror_and_version():
+    assert ot.ot_abi_version() == 1
+    assert ot.ot_strerror(0) == "ok"
+    for code in range(1, 6):
+        assert ot.ot_strerror(code) not in ("ok", "unknown status")
+    assert ot.ot_strerror(99) == "unknown status"
+    assert ot.ot_qlinear_workspace_size(64, 4096, 4096) == 0
+
+
+NULL = None
+
+
+def _qlinear(M, N, K, a_bits=8, w_bits=8):
+    return ot.lib().ot_qlinear(NULL, NULL, NULL, NULL, M, N, K, a_bits, w_bits, NULL, NULL,
+                               NULL, NULL)
+
+
+@pytest.mark.parametrize("args,code", [
+    ((4, 8, 32, 9, 8), ot.OT_EINVAL),      # a_bits out of range
+    ((4, 8, 32, 8, 1), ot.OT_EINVAL),      # w_bits out of range
+    ((-1, 8, 32, 8, 8), ot.OT_EINVAL),     # negative M
+    ((4, 8, 24, 8, 8), ot.OT_ESHAPE),      # K not a multiple of 16
+    ((4, 8, 0, 8, 8), ot.OT_ESHAPE),       # K = 0
+    ((4, 0, 32, 8, 8), ot.OT_ESHAPE),      # N = 0
+    ((4, 8, 133152, 8, 8), ot.OT_ERANGE),  # K * 127 * 127 >= 2^31
+    ((4, 8, 2234640, 6, 6), ot.OT_ERANGE),  # K * 31 * 31 >= 2^31
+    ((0, 8, 32, 8, 8), ot.OT_OK),          # M = 0 is a no-op
+    ((4, 8, 32, 8, 8), ot.OT_EINVAL),      # null pointers with work to do
+])
+def test_qlinear_argument_checks(args, code):
+    assert _qlinear(*args) == code
+
+
+def test_qlinear_w6a6_range_accepts_large_k():
+    # the same K that overflows at W8A8 is fine at W6A6, up to the null check
+    assert _qlinear(4, 8, 133152, 6, 6) == ot.OT_EINVAL
+
+
+def test_quantize_act_argument_checks():
+    L = ot.lib()
+    assert L.ot_quantize_act(NULL, 4, 24, 8, NULL, NULL, NULL, NULL) == ot.OT_ESHAPE
+    assert L.ot_quantize_act(NULL, 4, 32, 1, NULL, NULL, NULL, NULL) == ot.OT_EINVAL
+    assert L.ot_quantize_act(NULL, 0, 32, 8, NULL, NULL, NULL, NULL) == ot.OT_OK
+    assert L.ot_quantize_act(NULL, 4, 32, 8, NULL, NULL, NULL, NULL) == ot.OT_EINVAL
+    # misaligned (but non-null) pointers are rejected before any launch
+    assert L.ot_quantize_act(1, 4, 32, 8, 16, 16, 16, NULL) == ot.OT_EINVAL
+
+
+def test_calibrate_and_fold_argument_checks():
+    L = ot.lib()
+    assert L.ot_calibrate(NULL, 4, 32, 8, 1, NULL, NULL, NULL, NULL, NULL) == ot.OT_EINVAL
+    assert L.ot_calibrate(16, 0, 32, 8, 1, 16, 16, 16, 16, NULL) == ot.OT_ESHAPE
+    assert L.ot_calibrate(16, 4, 32, 9, 1, 16, 16, 16, 16, NULL) == ot.OT_EINVAL
+    assert L.ot_fold_weights(NULL, NULL, 8, 32, 8, NULL, NULL, NULL, NULL, NULL, NULL) == ot.OT_EINVAL
+    assert L.ot_fold_weights(16, NULL, 0, 32, 8, 16, 16, 16, 16, 16, NULL) == ot.OT_ESHAPE
+    assert L.ot_fold_weights(16, NULL, 8, 32, 0, 16, 16, 16, 16, 16, NULL) == ot.OT_EINVAL
+
+
+def test_binding_refuses_host_tensors():
+    import torch
+    x = torch.zeros((4, 32), dtype=torch.float16)
+    with pytest.raises(ValueError):
+        ot.ot_quantize_act(x, 8, torch.zeros(32), torch.zeros(32),
+                           torch.zeros((4, 32), dtype=torch.int8))

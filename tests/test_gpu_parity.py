@@ -1,0 +1,240 @@
+"""Parity of libot (through its C ABI) with the CPU oracle, element by element.
+
+Integer stages (minmax, z, s, inv_s, Wq, sW, Xq, acc) must be bit-exact; the
+compensated bias within 1 fp32 ulp (its fp64 sum order is unspecified); the
+fp16 output within 2 fp16 ulp and 1e-3 relative error.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import ot_oracle as O
+from paper_2406_18832_amd import ot, synth
+from tests._tol import assert_fp16_close, assert_fp32_within_ulps
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    ot.lib()
+    yield
+    torch.cuda.synchronize()
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def host(t):
+    torch.cuda.synchronize()
+    return t.cpu().numpy()
+
+
+def case(msg):
+    print(f"[case] {msg}", flush=True)
+
+
+# --------------------------------------------------------------------------
+# Calibration
+# --------------------------------------------------------------------------
+@pytest.mark.parametrize("a_bits", [8, 6, 3])
+def test_calibrate_streamed_batches_bit_exact(a_bits):
+    wl = synth.WORKLOADS["opt125m_w8a8"]
+    batches = list(synth.calibration_batches(wl, 0))
+    case(f"calibrate opt125m a_bits={a_bits}")
+    got = [host(t) for t in ot.calibrate(batches, a_bits)]
+    ref = O.calibrate(batches, a_bits)
+    for g, r, name in zip(got, ref, ["minmax", "z", "s", "inv_s"]):
+        assert np.array_equal(g.view(np.uint32), r.view(np.uint32)), name
+
+
+def test_calibrate_ragged_and_special_values():
+    r = np.random.default_rng(7)
+    K = 37  # not a multiple of anything the kernels tile by
+    a = r.normal(0, 3, size=(131, K)).astype(np.float16)
+    a[:, 0] = 2.0                  # constant channel -> s = 1
+    a[:, 1] = -0.0                 # all negative zeros -> +0
+    a[5, 2] = np.float16(65504)    # fp16 extremes
+    a[6, 2] = np.float16(-65504)
+    b = r.normal(1, 1, size=(3, K)).astype(np.float16)
+    case("calibrate ragged K=37")
+    got = [host(t) for t in ot.calibrate([a, b], 8)]
+    ref = O.calibrate([a, b], 8)
+    for g, rr, name in zip(got, ref, ["minmax", "z", "s", "inv_s"]):
+        assert np.array_equal(g.view(np.uint32), rr.view(np.uint32)), name
+
+
+@pytest.mark.parametrize("bad", [np.nan, np.inf, -np.inf])
+def test_calibrate_rejects_non_finite_then_recovers(bad):
+    x = np.ones((8, 32), dtype=np.float16)
+    x[3, 5] = bad
+    K = 32
+    minmax = torch.empty(2 * K, dtype=torch.float32, device="cuda")
+    z, s, inv_s = (torch.full((K,), 7.0, device="cuda") for _ in range(3))
+    case(f"calibrate non-finite {bad}")
+    with pytest.raises(ot.OTError) as e:
+        ot.ot_calibrate(dev(x), 8, True, minmax, z, s, inv_s)
+    assert e.value.code == ot.OT_ENONFINITE
+    assert torch.all(z == 7.0)  # outputs untouched
+    good = np.ones((8, 32), dtype=np.float16)
+    ot.ot_calibrate(dev(good), 8, True, minmax, z, s, inv_s)
+    assert torch.all(z == 1.0) and torch.all(s == 1.0)
+
+
+# --------------------------------------------------------------------------
+# Weight fold
+# --------------------------------------------------------------------------
+@pytest.mark.parametrize("w_bits,with_bias", [(8, True), (6, True), (4, False)])
+def test_fold_weights_parity(w_bits, with_bias):
+    wl = synth.WORKLOADS["opt125m_w8a8"]
+    _, z, s, _ = O.calibrate(list(synth.calibration_batches(wl, 0)), 8)
+    W = synth.weight(wl, 0).copy()
+    W[3] = 0  # an all-zero row
+    b = synth.bias(wl, 0) if with_bias else None
+    case(f"fold opt125m w_bits={w_bits} bias={with_bias}")
+    Wq, sW, bp = ot.fold_weights(dev(W), None if b is None else dev(b), w_bits, dev(z), dev(s))
+    rWq, rsW, rbp = O.fold_weights(W, b, z, s, w_bits)
+    assert np.array_equal(host(Wq), rWq)
+    assert np.array_equal(host(sW).view(np.uint32), rsW.view(np.uint32))
+    assert_fp32_within_ulps(host(bp), rbp, 1)
+
+
+def test_fold_rejects_non_finite():
+    W = np.ones((4, 32), dtype=np.float16)
+    W[2, 7] = np.inf
+    case("fold non-finite")
+    with pytest.raises(ot.OTError) as e:
+        ot.fold_weights(dev(W), None, 8, dev(np.zeros(32, np.float32)), dev(np.ones(32, np.float32)))
+    assert e.value.code == ot.OT_ENONFINITE
+    b = np.array([0, np.nan, 0, 0], dtype=np.float16)
+    with pytest.raises(ot.OTError):
+        ot.fold_weights(dev(np.ones((4, 32), np.float16)), dev(b), 8,
+                        dev(np.zeros(32, np.float32)), dev(np.ones(32, np.float32)))
+
+
+# --------------------------------------------------------------------------
+# Activation quantization
+# --------------------------------------------------------------------------
+@pytest.mark.parametrize("M,K,a_bits", [(16, 768, 8), (1, 16, 8), (3, 48, 6), (33, 1040, 8),
+                                        (70, 2064, 4), (257, 5120, 6)])
+def test_quantize_act_parity(M, K, a_bits):
+    r = np.random.default_rng(M * 7 + K)
+    x = (r.standard_normal((M, K)) * r.uniform(0.5, 30, size=K) + r.uniform(-5, 5, size=K))
+    x = x.astype(np.float16)
+    _, z, s, inv_s = O.calibrate([x[: max(1, M // 2)]], a_bits)  # later rows go out of range
+    case(f"quantize M={M} K={K} a_bits={a_bits}")
+    got = host(ot.quantize_act(dev(x), a_bits, dev(z), dev(inv_s)))
+    assert np.array_equal(got, O.quantize_act(x, z, inv_s, a_bits))
+
+
+def test_quantize_act_ties_and_clamps():
+    v = np.array([2.5, 3.5, -2.5, -0.5, 0.5, 1.5, 200.0, -200.0, 126.5, -127.5, 0.0, -0.0,
+                  65504, -65504, 1e-7, 6.5], dtype=np.float16)
+    x = np.tile(v, (2, 1))
+    K = x.shape[1]
+    z = np.zeros(K, np.float32)
+    one = np.ones(K, np.float32)
+    case("quantize ties")
+    got = host(ot.quantize_act(dev(x), 8, dev(z), dev(one)))
+    assert np.array_equal(got, O.quantize_act(x, z, one, 8))
+
+
+# --------------------------------------------------------------------------
+# Quantized linear on random codes: every tile shape, ragged edges
+# --------------------------------------------------------------------------
+def _random_qlinear_inputs(M, N, K, a_bits, w_bits, seed):
+    r = np.random.default_rng(seed)
+    qa, qw = O.qmax(a_bits), O.qmax(w_bits)
+    Xq = r.integers(-qa, qa + 1, size=(M, K)).astype(np.int8)
+    Wq = r.integers(-qw, qw + 1, size=(N, K)).astype(np.int8)
+    sW = (r.uniform(0.5, 2.0, size=N) * 1e-3).astype(np.float32)
+    bp = r.normal(0, 1, size=N).astype(np.float32)
+    return Xq, Wq, sW, bp
+
+
+QL_SHAPES = [
+    # decode kernel (M <= 64)
+    (1, 8, 16), (1, 300, 1040), (5, 772, 768), (16, 256, 4096), (17, 100, 400),
+    (32, 513, 128), (33, 64, 48), (64, 1000, 2064),
+    # prefill kernel
+    (65, 256, 128), (200, 300, 400), (256, 256, 256), (300, 772, 1040), (513, 129, 768),
+    (600, 1024, 4112),
+]
+
+
+@pytest.mark.parametrize("M,N,K", QL_SHAPES)
+def test_qlinear_parity_random_codes(M, N, K):
+    Xq, Wq, sW, bp = _random_qlinear_inputs(M, N, K, 8, 8, M * 1000 + N + K)
+    case(f"qlinear M={M} N={N} K={K}")
+    Y, acc = ot.qlinear(dev(Xq), dev(Wq), dev(sW), dev(bp), 8, 8, want_acc=True)
+    racc = O.int_gemm(Xq, Wq)
+    assert np.array_equal(host(acc), racc)
+    assert_fp16_close(host(Y), O.epilogue(racc, sW, bp))
+
+
+@pytest.mark.parametrize("M", [7, 64, 300])
+def test_qlinear_extreme_codes_near_int32_limit(M):
+    # K * 127 * 127 just below 2^31: the largest accumulators the ABI allows
+    K, N = 133136, 48
+    Xq = np.full((M, K), 127, dtype=np.int8)
+    Xq[1::2] = -127
+    Wq = np.full((N, K), 127, dtype=np.int8)
+    Wq[::3, ::2] = -127
+    sW = np.full(N, 1e-6, dtype=np.float32)
+    bp = np.zeros(N, dtype=np.float32)
+    case(f"qlinear extreme M={M} K={K}")
+    Y, acc = ot.qlinear(dev(Xq), dev(Wq), dev(sW), dev(bp), 8, 8, want_acc=True)
+    racc = O.int_gemm(Xq, Wq)
+    assert np.abs(racc.astype(np.int64)).max() == K * 127 * 127
+    assert np.array_equal(host(acc), racc)
+    assert_fp16_close(host(Y), O.epilogue(racc, sW, bp))
+
+
+def test_qlinear_output_overflow_is_inf():
+    M, N, K = 4, 8, 64
+    Xq = np.full((M, K), 127, dtype=np.int8)
+    Wq = np.full((N, K), 127, dtype=np.int8)
+    sW = np.full(N, 1.0, dtype=np.float32)  # 64 * 127^2 = 1032256 > 65504
+    bp = np.zeros(N, dtype=np.float32)
+    Y = host(ot.qlinear(dev(Xq), dev(Wq), dev(sW), dev(bp), 8, 8))
+    assert np.all(np.isposinf(Y))
+
+
+def test_qlinear_rejects_overflowing_k():
+    Xq = torch.zeros((2, 133152), dtype=torch.int8, device="cuda")
+    Wq = torch.zeros((4, 133152), dtype=torch.int8, device="cuda")
+    with pytest.raises(ot.OTError) as e:
+        ot.qlinear(Xq, Wq, torch.ones(4, device="cuda"), torch.zeros(4, device="cuda"), 8, 8)
+    assert e.value.code == ot.OT_ERANGE
+
+
+def test_qlinear_is_deterministic():
+    Xq, Wq, sW, bp = _random_qlinear_inputs(512, 768, 1024, 8, 8, 3)
+    args = (dev(Xq), dev(Wq), dev(sW), dev(bp), 8, 8)
+    y1 = host(ot.qlinear(*args))
+    y2 = host(ot.qlinear(*args))
+    assert y1.tobytes() == y2.tobytes()
+
+
+# --------------------------------------------------------------------------
+# End to end on the OPT-125m-shaped workload
+# --------------------------------------------------------------------------
+@pytest.mark.parametrize("a_bits,w_bits", [(8, 8), (6, 6)])
+def test_pipeline_opt125m(a_bits, w_bits):
+    wl = synth.WORKLOADS["opt125m_w8a8"]
+    batches = list(synth.calibration_batches(wl, 0))
+    X = synth.activations(wl, 0, wl.M)
+    W = synth.weight(wl, 0)
+    b = synth.bias(wl, 0)
+    case(f"pipeline opt125m W{w_bits}A{a_bits}")
+    ref = O.pipeline(X, W, b, batches, a_bits, w_bits)
+    _, z, s, inv_s = ot.calibrate(batches, a_bits)
+    Wq, sW, bp = ot.fold_weights(dev(W), dev(b), w_bits, z, s)
+    Xq = ot.quantize_act(dev(X), a_bits, z, inv_s)
+    Y, acc = ot.qlinear(Xq, Wq, sW, bp, a_bits, w_bits, want_acc=True)
+    assert np.array_equal(host(Xq), ref["Xq"])
+    assert np.array_equal(host(Wq), ref["Wq"])
+    assert np.array_equal(host(acc), ref["acc"])
+    assert_fp16_close(host(Y), ref["Y"])
