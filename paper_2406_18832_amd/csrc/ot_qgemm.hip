@@ -419,24 +419,66 @@ hipError_t launch_prefill(const int8_t *Xq, const int8_t *Wq, const float *sW, c
 }
 
 // ---------------------------------------------------------------------------
-// Decode (M <= 64): weight-streaming GEMV-like kernel on v_mfma_i32_16x16x64_i8
+// Decode (M <= 64): weight-streaming kernel on v_mfma_i32_16x16x64_i8
 // ---------------------------------------------------------------------------
 // HBM-bound on the weight bytes.  A workgroup owns 16*RB weight rows and all
-// tokens (MB blocks of 16, zero-padded), and its kWaves waves split K in
-// 64-byte steps, interleaved, so that together they stream whole cache lines
-// of each row.  Each lane loads 16 bytes of one weight row per step (a wave
-// covers 16 rows x 64 contiguous bytes), and the matching 16 bytes of each
-// token row, which stay in L2 across workgroups.  U steps are kept in flight
-// per wave.  The partial accumulators of the waves are summed in LDS and the
-// epilogue is fused.
-constexpr int kDecWaves = 8;
+// tokens (MB blocks of 16, zero-padded); its NW waves split K into runs of U
+// consecutive 64-byte steps, interleaved wave by wave.  Per step a lane loads
+// 16 bytes of each of its RB weight rows (a wave covers 16 rows x 64
+// contiguous bytes per load) and the matching 16 bytes of each of its MB
+// token rows (L2-resident; each token load feeds RB MFMAs).  A wave's U loads
+// of a row are back to back in K, so each 128-byte line is requested by one
+// wave at once rather than half by each of two.  The U steps of a run are
+// one batch; batches are double-buffered in registers, so the
+// next batch's loads are in flight while the current one feeds the matrix
+// cores.  Loads past the end of K or of the rows read zeros (buffer bounds),
+// so every wave runs the same branch-free batch count.  The waves' partial
+// accumulators are summed in LDS and the epilogue is fused.
+template <int MB, int RB, int NW, int U>
+struct DecodeCfg {
+  static constexpr int kStepBytes = 64;
+  static constexpr int kBatch = NW * U;  // steps consumed per batch by the workgroup
+  static constexpr int kLds = RB * MB * 64 * 16;
+  static_assert(kLds <= 64 * 1024, "LDS");
+};
+
+template <int MB, int RB, int NW, int U>
+__device__ __forceinline__ void decode_load(__amdgpu_buffer_rsrc_t rw, __amdgpu_buffer_rsrc_t rx,
+                                            const uint32_t *offw, const uint32_t *offx, int s,
+                                            int kchunk, int K, v4i (&w)[U][RB], v4i (&x)[U][MB]) {
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const int st = s + u;  // U consecutive steps: whole cache lines per wave
+    // Past the end of the row, bit 31 pushes the offset out of the resource
+    // (valid offsets stay below 2^30), so the load returns zeros.  Written as
+    // arithmetic: a select here gets turned into a branch around each load.
+    const uint32_t kb = (uint32_t)st * 64u | ((uint32_t)(st * 64 + kchunk >= K) << 31);
+#pragma unroll
+    for (int i = 0; i < RB; ++i) w[u][i] = __builtin_amdgcn_raw_buffer_load_b128(rw, offw[i] + kb, 0, 0);
+#pragma unroll
+    for (int j = 0; j < MB; ++j) x[u][j] = __builtin_amdgcn_raw_buffer_load_b128(rx, offx[j] + kb, 0, 0);
+  }
+}
 
 template <int MB, int RB, int U>
-__global__ __launch_bounds__(64 * kDecWaves) void qgemm_decode_kernel(
+__device__ __forceinline__ void decode_mfma(v4i (&acc)[RB][MB], const v4i (&w)[U][RB],
+                                            const v4i (&x)[U][MB]) {
+#pragma unroll
+  for (int u = 0; u < U; ++u)
+#pragma unroll
+    for (int i = 0; i < RB; ++i)
+#pragma unroll
+      for (int j = 0; j < MB; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(w[u][i], x[u][j], acc[i][j], 0, 0, 0);
+}
+
+template <int MB, int RB, int NW, int U>
+__global__ __launch_bounds__(64 * NW) void qgemm_decode_kernel(
     const int8_t *__restrict__ Xq, const int8_t *__restrict__ Wq, const float *__restrict__ sW,
     const float *__restrict__ bp, int M, int N, int K, uint16_t *__restrict__ Y,
     int32_t *__restrict__ acc_out) {
-  __shared__ v4i red[kDecWaves][RB][MB][64];
+  using C = DecodeCfg<MB, RB, NW, U>;
+  __shared__ v4i red[RB][MB][64];
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int n0 = blockIdx.x * 16 * RB;
@@ -444,12 +486,11 @@ __global__ __launch_bounds__(64 * kDecWaves) void qgemm_decode_kernel(
   const __amdgpu_buffer_rsrc_t rw = make_rsrc(Wq + (int64_t)n0 * K, (uint32_t)(rows_w * K));
   const __amdgpu_buffer_rsrc_t rx = make_rsrc(Xq, (uint32_t)(M * K));
   const int r16 = lane & 15, c4 = lane >> 4;
-  // byte offsets of this lane's 16-byte piece within a 64-byte step
   uint32_t offw[RB], offx[MB];
 #pragma unroll
   for (int i = 0; i < RB; ++i) offw[i] = (uint32_t)((i * 16 + r16) * K + c4 * 16);
 #pragma unroll
-  for (int i = 0; i < MB; ++i) offx[i] = (uint32_t)((i * 16 + r16) * K + c4 * 16);
+  for (int j = 0; j < MB; ++j) offx[j] = (uint32_t)((j * 16 + r16) * K + c4 * 16);
 
   v4i acc[RB][MB];
 #pragma unroll
@@ -458,54 +499,48 @@ __global__ __launch_bounds__(64 * kDecWaves) void qgemm_decode_kernel(
     for (int j = 0; j < MB; ++j) acc[i][j] = v4i{};
 
   const int steps = (K + 63) / 64;
-  for (int s0 = wave; s0 < steps; s0 += kDecWaves * U) {
-    v4i w[U][RB], x[U][MB];
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int s = s0 + u * kDecWaves;
-      const int k = s * 64 + c4 * 16;
-      const bool ok = s < steps && k < K;
-#pragma unroll
-      for (int i = 0; i < RB; ++i)
-        w[u][i] = __builtin_amdgcn_raw_buffer_load_b128(rw, ok ? offw[i] + (uint32_t)(s * 64) : kOobOffset, 0, 0);
-#pragma unroll
-      for (int j = 0; j < MB; ++j)
-        x[u][j] = __builtin_amdgcn_raw_buffer_load_b128(rx, ok ? offx[j] + (uint32_t)(s * 64) : kOobOffset, 0, 0);
-    }
-#pragma unroll
-    for (int u = 0; u < U; ++u)
-#pragma unroll
-      for (int i = 0; i < RB; ++i)
-#pragma unroll
-        for (int j = 0; j < MB; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(w[u][i], x[u][j], acc[i][j], 0, 0, 0);
+  const int batches = (steps + C::kBatch - 1) / C::kBatch;  // same for every wave
+  v4i wa[U][RB], xa[U][MB], wb[U][RB], xb[U][MB];
+  int s = wave * U;  // batch b of wave w covers steps b*NW*U + w*U + [0, U)
+  decode_load<MB, RB, NW, U>(rw, rx, offw, offx, s, c4 * 16, K, wa, xa);
+  for (int b = 0; b < batches; b += 2) {
+    decode_load<MB, RB, NW, U>(rw, rx, offw, offx, s + C::kBatch, c4 * 16, K, wb, xb);
+    decode_mfma<MB, RB, U>(acc, wa, xa);
+    if (b + 1 >= batches) break;
+    decode_load<MB, RB, NW, U>(rw, rx, offw, offx, s + 2 * C::kBatch, c4 * 16, K, wa, xa);
+    decode_mfma<MB, RB, U>(acc, wb, xb);
+    s += 2 * C::kBatch;
   }
 
+  // Sum the waves' partial accumulators in one LDS buffer, one wave at a
+  // time (a small buffer lets several workgroups share a CU).
+  for (int w = 0; w < NW; ++w) {
+    if (wave == w) {
 #pragma unroll
-  for (int i = 0; i < RB; ++i)
+      for (int i = 0; i < RB; ++i)
 #pragma unroll
-    for (int j = 0; j < MB; ++j) red[wave][i][j][lane] = acc[i][j];
-  __syncthreads();
+        for (int j = 0; j < MB; ++j) red[i][j][lane] = (w == 0 ? v4i{} : red[i][j][lane]) + acc[i][j];
+    }
+    __syncthreads();
+  }
   // 16x16 output block, 4 values per lane: lane l holds column (l mod 16) and
   // rows 4*(l/16) + r.  Rows are channels, columns tokens.
-  for (int t = wave; t < RB * MB; t += kDecWaves) {
+  for (int t = wave; t < RB * MB; t += NW) {
     const int i = t / MB, j = t % MB;
-    v4i sum = v4i{};
-#pragma unroll
-    for (int w = 0; w < kDecWaves; ++w) sum += red[w][i][j][lane];
+    const v4i sum = red[i][j][lane];
     const int64_t m = j * 16 + r16;
     const int64_t n = n0 + i * 16 + 4 * c4;
     store4(Y, acc_out, sW, bp, m, n, M, N, sum[0], sum[1], sum[2], sum[3]);
   }
 }
 
-template <int MB, int RB, int U>
+template <int MB, int RB, int NW, int U>
 hipError_t launch_decode(const int8_t *Xq, const int8_t *Wq, const float *sW, const float *bp,
                          int64_t M, int64_t N, int64_t K, uint16_t *Y, int32_t *acc_out,
                          hipStream_t st) {
   const unsigned grid = (unsigned)((N + 16 * RB - 1) / (16 * RB));
-  qgemm_decode_kernel<MB, RB, U><<<grid, 64 * kDecWaves, 0, st>>>(
-      Xq, Wq, sW, bp, (int)M, (int)N, (int)K, Y, acc_out);
+  qgemm_decode_kernel<MB, RB, NW, U><<<grid, 64 * NW, 0, st>>>(Xq, Wq, sW, bp, (int)M, (int)N,
+                                                             (int)K, Y, acc_out);
   return hipGetLastError();
 }
 
@@ -516,9 +551,17 @@ using namespace detail;
 hipError_t launch_qgemm(const int8_t *Xq, const int8_t *Wq, const float *sW, const float *bprime,
                         int64_t M, int64_t N, int64_t K, uint16_t *Y, int32_t *acc_out,
                         hipStream_t st) {
-  if (M <= 16) return launch_decode<1, 1, 4>(Xq, Wq, sW, bprime, M, N, K, Y, acc_out, st);
-  if (M <= 32) return launch_decode<2, 1, 4>(Xq, Wq, sW, bprime, M, N, K, Y, acc_out, st);
-  if (M <= 64) return launch_decode<4, 1, 2>(Xq, Wq, sW, bprime, M, N, K, Y, acc_out, st);
+  // Decode: rows per workgroup (16*RB) trade token-row reuse (large RB)
+  // against enough workgroups to fill the GPU (small RB); measured on the
+  // OPT-30B shapes at 1, 8, 32 and 64 tokens.
+  const bool wide = N >= 16384;
+  if (M <= 16) return launch_decode<1, 2, 4, 4>(Xq, Wq, sW, bprime, M, N, K, Y, acc_out, st);
+  if (M <= 32)
+    return wide ? launch_decode<2, 8, 8, 1>(Xq, Wq, sW, bprime, M, N, K, Y, acc_out, st)
+                : launch_decode<2, 2, 4, 4>(Xq, Wq, sW, bprime, M, N, K, Y, acc_out, st);
+  if (M <= 64)
+    return wide ? launch_decode<4, 4, 8, 1>(Xq, Wq, sW, bprime, M, N, K, Y, acc_out, st)
+                : launch_decode<4, 2, 8, 2>(Xq, Wq, sW, bprime, M, N, K, Y, acc_out, st);
   return launch_prefill<256, 256, 128, 4, 2, 2>(Xq, Wq, sW, bprime, M, N, K, Y, acc_out, st);
 }
 
