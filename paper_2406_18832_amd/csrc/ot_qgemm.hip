@@ -18,6 +18,8 @@
 // as the A and B lanes that meet use the same assignment.  Every lane here
 // loads 16 contiguous K bytes for its row, picked identically on both sides,
 // so the product is the plain dot product whatever the hardware's order.
+#include <type_traits>
+
 #include "ot_common.h"
 
 namespace ot {
@@ -140,20 +142,13 @@ __device__ __forceinline__ void sched_interleave() {
   if (kMfma > kPaired) __builtin_amdgcn_sched_group_barrier(kMask_MFMA, kMfma - kPaired, 0);
 }
 
-// s_waitcnt immediate (gfx9 encoding) waiting for at most n vector-memory
-// operations, leaving the other counters unconstrained.
-__device__ __forceinline__ void wait_vmcnt_le(int n) {
-  // the argument must fold to a constant at every call site
-  switch (n) {
-    case 0: __builtin_amdgcn_s_waitcnt(0x0F70); break;
-    case 4: __builtin_amdgcn_s_waitcnt(0x0F74); break;
-    case 8: __builtin_amdgcn_s_waitcnt(0x0F78); break;
-    case 12: __builtin_amdgcn_s_waitcnt(0x0F7C); break;
-    case 16: __builtin_amdgcn_s_waitcnt(0x4F70); break;
-    case 24: __builtin_amdgcn_s_waitcnt(0x4F78); break;
-    case 32: __builtin_amdgcn_s_waitcnt(0x8F70); break;
-    default: __builtin_amdgcn_s_waitcnt(0x0F70); break;
-  }
+// s_waitcnt (gfx9 encoding) waiting until at most N vector-memory operations
+// are outstanding, leaving the other counters unconstrained.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N <= 63, "vmcnt range");
+  constexpr int kImm = (N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8);
+  __builtin_amdgcn_s_waitcnt(kImm);
 }
 
 // The kernel body lives in a device function: hipcc drops the host stub of a
@@ -269,7 +264,7 @@ __device__ __forceinline__ void prefill_body(
   // of loads in flight and one fixed wait, with no branches in the loop.
 #pragma unroll
   for (int t = 0; t < S - 1; ++t) issue_tile(t);
-  wait_vmcnt_le((S - 2) * C::kLoads);  // tile 0 has landed
+  wait_vmcnt<(S - 2) * C::kLoads>();  // tile 0 has landed
   lds_barrier();
   issue_tile(S - 1);
   read_frags(0, 0, 0);
@@ -290,14 +285,14 @@ __device__ __forceinline__ void prefill_body(
     // wait, so the reads have that long to land.
     __builtin_amdgcn_sched_barrier(0);
     __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
-    wait_vmcnt_le((S - 2) * C::kLoads);
+    wait_vmcnt<(S - 2) * C::kLoads>();
     lds_barrier();
     issue_tile(kt + S);
     read_frags(kt + 1, 0, 0);
     mfmas(1);
     sched_interleave<C::kFN + C::kFM, C::kFN * C::kFM, C::kLoads>();
   }
-  wait_vmcnt_le(0);
+  wait_vmcnt<0>();
 
   // ---- epilogue ----------------------------------------------------------------
   // 32x32 output block, 16 values per lane: lane l holds column (l mod 32)
@@ -329,7 +324,7 @@ __device__ __forceinline__ void prefill_body(
   static_assert((kUnits & (kUnits - 1)) == 0 && kUnits >= 16, "row of a power-of-two units");
   static_assert(C::kWaves * C::kTM * C::kTN * 2 <= S * C::kStage, "epilogue tile fits the ring");
   __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): this wave's last reads
-  wait_vmcnt_le(0);                     // the trailing out-of-range tiles
+  wait_vmcnt<0>();                     // the trailing out-of-range tiles
   lds_barrier();                        // every wave is done with the ring
   uint16_t *tile = reinterpret_cast<uint16_t *>(smem) + wave * (C::kTM * C::kTN);
   const int nw0 = n0 + wn * C::kTN;   // first channel of this wave
@@ -419,128 +414,207 @@ hipError_t launch_prefill(const int8_t *Xq, const int8_t *Wq, const float *sW, c
 }
 
 // ---------------------------------------------------------------------------
-// Decode (M <= 64): weight-streaming kernel on v_mfma_i32_16x16x64_i8
+// Decode: per-wave LDS-DMA weight rings
 // ---------------------------------------------------------------------------
-// HBM-bound on the weight bytes.  A workgroup owns 16*RB weight rows and all
-// tokens (MB blocks of 16, zero-padded); its NW waves split K into runs of U
-// consecutive 64-byte steps, interleaved wave by wave.  Per step a lane loads
-// 16 bytes of each of its RB weight rows (a wave covers 16 rows x 64
-// contiguous bytes per load) and the matching 16 bytes of each of its MB
-// token rows (L2-resident; each token load feeds RB MFMAs).  A wave's U loads
-// of a row are back to back in K, so each 128-byte line is requested by one
-// wave at once rather than half by each of two.  The U steps of a run are
-// one batch; batches are double-buffered in registers, so the
-// next batch's loads are in flight while the current one feeds the matrix
-// cores.  Loads past the end of K or of the rows read zeros (buffer bounds),
-// so every wave runs the same branch-free batch count.  The waves' partial
-// accumulators are summed in LDS and the epilogue is fused.
-template <int MB, int RB, int NW, int U>
-struct DecodeCfg {
-  static constexpr int kStepBytes = 64;
-  static constexpr int kBatch = NW * U;  // steps consumed per batch by the workgroup
-  static constexpr int kLds = RB * MB * 64 * 16;
-  static_assert(kLds <= 64 * 1024, "LDS");
+// A workgroup owns 16*RBW weight rows; its KSW waves each take a contiguous
+// slice of K and run independently (no barrier until the final reduction).
+// A wave's weight slice streams through a private ring of S LDS stages, each
+// [16*RBW rows][BKD bytes], filled by buffer load-to-LDS (no registers held
+// while the loads are in flight, so many kilobytes per wave can be
+// outstanding); each 1 KiB load covers 1024/BKD whole rows of BKD
+// contiguous bytes.  Chunk c (16
+// bytes) of row r sits at chunk c ^ (r mod 16) of that row, so the fragment
+// reads (16 rows, one chunk each) are free of bank conflicts.  Token rows are
+// L2-resident and are loaded straight into registers one stage ahead.  With
+// KSW > 1 the waves' partial sums are added in LDS at the end.
+template <int TM, int MB, int RBW, int BKD, int S>
+struct Decode2Cfg {
+  static constexpr int kRows = TM * RBW;           // weight rows per workgroup
+  static constexpr int kChunks = BKD / 16;         // 16-byte chunks per row
+  static constexpr int kStepB = TM == 16 ? 64 : 32;  // K bytes per MFMA
+  static constexpr int kSteps = BKD / kStepB;      // MFMA K steps per stage
+  static constexpr int kStage = kRows * BKD;       // bytes
+  static constexpr int kDma = kStage / 1024;       // loads per stage
+  static constexpr int kXLoads = kSteps * MB;      // token loads per stage
+  static_assert(TM == 16 || TM == 32, "16x16x64 or 32x32x32 MFMA");
+  static_assert(BKD == 256, "16 chunks per row (the swizzle period)");
+  static_assert(kStage % 1024 == 0 && kDma + kXLoads <= 63, "vmcnt range");
 };
 
-template <int MB, int RB, int NW, int U>
-__device__ __forceinline__ void decode_load(__amdgpu_buffer_rsrc_t rw, __amdgpu_buffer_rsrc_t rx,
-                                            const uint32_t *offw, const uint32_t *offx, int s,
-                                            int kchunk, int K, v4i (&w)[U][RB], v4i (&x)[U][MB]) {
+// TM = 16: v_mfma_i32_16x16x64_i8, lane l = (row l%16, 16-byte chunk l/16 of
+//          a 64-byte step); MB token blocks of 16.
+// TM = 32: v_mfma_i32_32x32x32_i8, lane l = (row l%32, chunk l/32 of a
+//          32-byte step); MB token blocks of 32 (twice the work per
+//          instruction, used from 32 tokens up).
+template <int TM, int MB, int RBW, int BKD, int S, int KSW>
+__device__ __forceinline__ void decode2_body(
+    int8_t *smem, const int8_t *__restrict__ Xq, const int8_t *__restrict__ Wq,
+    const float *__restrict__ sW, const float *__restrict__ bp, int M, int N, int K,
+    uint16_t *__restrict__ Y, int32_t *__restrict__ acc_out) {
+  using C = Decode2Cfg<TM, MB, RBW, BKD, S>;
+  using acc_t = typename std::conditional<TM == 16, v4i, v16i>::type;
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  int8_t *ring = smem + wave * (S * C::kStage);
+  const int n0 = blockIdx.x * C::kRows;
+  const int rows_w = min(C::kRows, N - n0);
+  const __amdgpu_buffer_rsrc_t rw = make_rsrc(Wq + (int64_t)n0 * K, (uint32_t)(rows_w * K));
+  const __amdgpu_buffer_rsrc_t rx = make_rsrc(Xq, (uint32_t)(M * K));
+  const int fr = lane % TM, fc = lane / TM;  // MFMA row and chunk-within-step
+
+  // DMA lane mapping: load d of a stage fills rows 4d..4d+3 (BKD = 256);
+  // lane i lands at row 4d + i/16, physical chunk i%16, and fetches the
+  // logical chunk stored there.
+  const int drow = lane >> 4;  // row 4d + drow
+  // token fragment offsets: lane (fr, fc) reads token j*TM + fr at byte fc*16
+  uint32_t offx[MB];
 #pragma unroll
-  for (int u = 0; u < U; ++u) {
-    const int st = s + u;  // U consecutive steps: whole cache lines per wave
-    // Past the end of the row, bit 31 pushes the offset out of the resource
-    // (valid offsets stay below 2^30), so the load returns zeros.  Written as
-    // arithmetic: a select here gets turned into a branch around each load.
-    const uint32_t kb = (uint32_t)st * 64u | ((uint32_t)(st * 64 + kchunk >= K) << 31);
+  for (int j = 0; j < MB; ++j) offx[j] = (uint32_t)((j * TM + fr) * K + fc * 16);
+  // weight fragment LDS offsets within a stage for step t, row block 0
+  constexpr int kCpS = C::kStepB / 16;  // chunks per step
+  int frag[C::kSteps];
 #pragma unroll
-    for (int i = 0; i < RB; ++i) w[u][i] = __builtin_amdgcn_raw_buffer_load_b128(rw, offw[i] + kb, 0, 0);
+  for (int t = 0; t < C::kSteps; ++t) frag[t] = fr * BKD + 16 * ((kCpS * t + fc) ^ (fr & 15));
+
+  // this wave's slice of K: stages [s0, s0 + nst)
+  const int nst_all = (K + BKD - 1) / BKD;
+  const int per = (nst_all + KSW - 1) / KSW;
+  const int s0 = wave * per;
+  const int nst = max(0, min(per, nst_all - s0));
+
+  // st is relative to the slice; stages past it (or past K) read zeros
+  auto issue_w = [&](int st) {
+    int8_t *dst = ring + (st % S) * C::kStage;
+    const int k0 = (st < nst ? s0 + st : nst_all) * BKD;
 #pragma unroll
-    for (int j = 0; j < MB; ++j) x[u][j] = __builtin_amdgcn_raw_buffer_load_b128(rx, offx[j] + kb, 0, 0);
+    for (int d = 0; d < C::kDma; ++d) {
+      const int row = 4 * d + drow;
+      const int ch = (lane & 15) ^ (row & 15);
+      const int kk = k0 + ch * 16;
+      const uint32_t off = (uint32_t)(row * K + kk) | ((uint32_t)(kk >= K) << 31);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (lds_void *)(dst + d * 1024), 16, off, 0, 0, 0);
+    }
+  };
+  auto issue_x = [&](int st, v4i (&xb)[C::kSteps][MB]) {
+    const int k0 = (st < nst ? s0 + st : nst_all) * BKD;
+#pragma unroll
+    for (int t = 0; t < C::kSteps; ++t) {
+      const int kk = k0 + t * C::kStepB + fc * 16;
+      const uint32_t kb = (uint32_t)(k0 + t * C::kStepB) | ((uint32_t)(kk >= K) << 31);
+#pragma unroll
+      for (int j = 0; j < MB; ++j) xb[t][j] = __builtin_amdgcn_raw_buffer_load_b128(rx, offx[j] + kb, 0, 0);
+    }
+  };
+
+  acc_t acc[RBW][MB];
+#pragma unroll
+  for (int i = 0; i < RBW; ++i)
+#pragma unroll
+    for (int j = 0; j < MB; ++j) acc[i][j] = acc_t{};
+  v4i xa[C::kSteps][MB], xb[C::kSteps][MB];
+
+  auto compute = [&](int st, const v4i (&xs)[C::kSteps][MB]) {
+    const int8_t *src = ring + (st % S) * C::kStage;
+#pragma unroll
+    for (int t = 0; t < C::kSteps; ++t) {
+      v4i wf[RBW];
+#pragma unroll
+      for (int i = 0; i < RBW; ++i)
+        wf[i] = *reinterpret_cast<const v4i *>(src + i * TM * BKD + frag[t]);
+#pragma unroll
+      for (int i = 0; i < RBW; ++i)
+#pragma unroll
+        for (int j = 0; j < MB; ++j) {
+          if constexpr (TM == 16)
+            acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(wf[i], xs[t][j], acc[i][j], 0, 0, 0);
+          else
+            acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(wf[i], xs[t][j], acc[i][j], 0, 0, 0);
+        }
+    }
+  };
+
+  // Stages past the end of K are issued as out-of-range loads (zeros), so
+  // every iteration keeps the same number of loads in flight.
+#pragma unroll
+  for (int st = 0; st < S - 1; ++st) issue_w(st);
+  issue_x(0, xa);
+  // In-flight order (oldest first) when stage st is consumed: ... W(st),
+  // ..., X(st), W(st+S-1), X(st+1); so W(st) and X(st) have landed once at
+  // most kDma + kXLoads loads remain outstanding.
+  for (int st = 0; st < nst; st += 2) {
+    __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): slot (st-1)%S fully read
+    issue_w(st + S - 1);
+    issue_x(st + 1, xb);
+    wait_vmcnt<C::kDma + C::kXLoads>();
+    compute(st, xa);
+    if (st + 1 >= nst) break;
+    __builtin_amdgcn_s_waitcnt(0xC07F);
+    issue_w(st + S);
+    issue_x(st + 2, xa);
+    wait_vmcnt<C::kDma + C::kXLoads>();
+    compute(st + 1, xb);
   }
+  wait_vmcnt<0>();
+
+  if constexpr (KSW > 1) {
+    // add the waves' partial sums in LDS (over the idle rings), one wave at
+    // a time, then wave 0 holds the total
+    static_assert(RBW * MB * sizeof(acc_t) * 64 <= S * C::kStage, "reduction buffer fits a ring");
+    acc_t *red = reinterpret_cast<acc_t *>(smem);
+    __syncthreads();
+    for (int w = KSW - 1; w >= 1; --w) {
+      if (wave == w) {
+#pragma unroll
+        for (int i = 0; i < RBW; ++i)
+#pragma unroll
+          for (int j = 0; j < MB; ++j) {
+            acc_t &slot = red[(i * MB + j) * 64 + lane];
+            slot = (w == KSW - 1 ? acc_t{} : slot) + acc[i][j];
+          }
+      }
+      __syncthreads();
+    }
+    if (wave != 0) return;
+#pragma unroll
+    for (int i = 0; i < RBW; ++i)
+#pragma unroll
+      for (int j = 0; j < MB; ++j) acc[i][j] += red[(i * MB + j) * 64 + lane];
+  }
+  // Output blocks: columns are tokens, rows channels.  16x16: lane l holds
+  // column l%16, rows 4*(l/16) + r.  32x32: lane l holds column l%32 and rows
+  // 8*(r/4) + 4*(l/32) + (r%4), so registers 4g..4g+3 are 4 consecutive rows.
+#pragma unroll
+  for (int i = 0; i < RBW; ++i)
+#pragma unroll
+    for (int j = 0; j < MB; ++j) {
+      const int64_t m = j * TM + fr;
+      constexpr int kGroups = TM == 16 ? 1 : 4;  // 4-row groups per lane
+#pragma unroll
+      for (int g = 0; g < kGroups; ++g) {
+        const int64_t n = n0 + i * TM + (TM == 16 ? 4 * fc : 8 * g + 4 * fc);
+        store4(Y, acc_out, sW, bp, m, n, M, N, acc[i][j][4 * g], acc[i][j][4 * g + 1],
+               acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]);
+      }
+    }
 }
 
-template <int MB, int RB, int U>
-__device__ __forceinline__ void decode_mfma(v4i (&acc)[RB][MB], const v4i (&w)[U][RB],
-                                            const v4i (&x)[U][MB]) {
-#pragma unroll
-  for (int u = 0; u < U; ++u)
-#pragma unroll
-    for (int i = 0; i < RB; ++i)
-#pragma unroll
-      for (int j = 0; j < MB; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(w[u][i], x[u][j], acc[i][j], 0, 0, 0);
-}
-
-template <int MB, int RB, int NW, int U>
-__global__ __launch_bounds__(64 * NW) void qgemm_decode_kernel(
+template <int TM, int MB, int RBW, int BKD, int S, int KSW>
+__global__ __launch_bounds__(64 * KSW) void qgemm_decode2_kernel(
     const int8_t *__restrict__ Xq, const int8_t *__restrict__ Wq, const float *__restrict__ sW,
     const float *__restrict__ bp, int M, int N, int K, uint16_t *__restrict__ Y,
     int32_t *__restrict__ acc_out) {
-  using C = DecodeCfg<MB, RB, NW, U>;
-  __shared__ v4i red[RB][MB][64];
-  const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
-  const int n0 = blockIdx.x * 16 * RB;
-  const int rows_w = min(16 * RB, N - n0);
-  const __amdgpu_buffer_rsrc_t rw = make_rsrc(Wq + (int64_t)n0 * K, (uint32_t)(rows_w * K));
-  const __amdgpu_buffer_rsrc_t rx = make_rsrc(Xq, (uint32_t)(M * K));
-  const int r16 = lane & 15, c4 = lane >> 4;
-  uint32_t offw[RB], offx[MB];
-#pragma unroll
-  for (int i = 0; i < RB; ++i) offw[i] = (uint32_t)((i * 16 + r16) * K + c4 * 16);
-#pragma unroll
-  for (int j = 0; j < MB; ++j) offx[j] = (uint32_t)((j * 16 + r16) * K + c4 * 16);
-
-  v4i acc[RB][MB];
-#pragma unroll
-  for (int i = 0; i < RB; ++i)
-#pragma unroll
-    for (int j = 0; j < MB; ++j) acc[i][j] = v4i{};
-
-  const int steps = (K + 63) / 64;
-  const int batches = (steps + C::kBatch - 1) / C::kBatch;  // same for every wave
-  v4i wa[U][RB], xa[U][MB], wb[U][RB], xb[U][MB];
-  int s = wave * U;  // batch b of wave w covers steps b*NW*U + w*U + [0, U)
-  decode_load<MB, RB, NW, U>(rw, rx, offw, offx, s, c4 * 16, K, wa, xa);
-  for (int b = 0; b < batches; b += 2) {
-    decode_load<MB, RB, NW, U>(rw, rx, offw, offx, s + C::kBatch, c4 * 16, K, wb, xb);
-    decode_mfma<MB, RB, U>(acc, wa, xa);
-    if (b + 1 >= batches) break;
-    decode_load<MB, RB, NW, U>(rw, rx, offw, offx, s + 2 * C::kBatch, c4 * 16, K, wa, xa);
-    decode_mfma<MB, RB, U>(acc, wb, xb);
-    s += 2 * C::kBatch;
-  }
-
-  // Sum the waves' partial accumulators in one LDS buffer, one wave at a
-  // time (a small buffer lets several workgroups share a CU).
-  for (int w = 0; w < NW; ++w) {
-    if (wave == w) {
-#pragma unroll
-      for (int i = 0; i < RB; ++i)
-#pragma unroll
-        for (int j = 0; j < MB; ++j) red[i][j][lane] = (w == 0 ? v4i{} : red[i][j][lane]) + acc[i][j];
-    }
-    __syncthreads();
-  }
-  // 16x16 output block, 4 values per lane: lane l holds column (l mod 16) and
-  // rows 4*(l/16) + r.  Rows are channels, columns tokens.
-  for (int t = wave; t < RB * MB; t += NW) {
-    const int i = t / MB, j = t % MB;
-    const v4i sum = red[i][j][lane];
-    const int64_t m = j * 16 + r16;
-    const int64_t n = n0 + i * 16 + 4 * c4;
-    store4(Y, acc_out, sW, bp, m, n, M, N, sum[0], sum[1], sum[2], sum[3]);
-  }
+  __shared__ __attribute__((aligned(1024)))
+  int8_t smem[KSW * S * Decode2Cfg<TM, MB, RBW, BKD, S>::kStage];
+  decode2_body<TM, MB, RBW, BKD, S, KSW>(smem, Xq, Wq, sW, bp, M, N, K, Y, acc_out);
 }
 
-template <int MB, int RB, int NW, int U>
-hipError_t launch_decode(const int8_t *Xq, const int8_t *Wq, const float *sW, const float *bp,
-                         int64_t M, int64_t N, int64_t K, uint16_t *Y, int32_t *acc_out,
-                         hipStream_t st) {
-  const unsigned grid = (unsigned)((N + 16 * RB - 1) / (16 * RB));
-  qgemm_decode_kernel<MB, RB, NW, U><<<grid, 64 * NW, 0, st>>>(Xq, Wq, sW, bp, (int)M, (int)N,
-                                                             (int)K, Y, acc_out);
+template <int TM, int MB, int RBW, int BKD, int S, int KSW = 1>
+hipError_t launch_decode2(const int8_t *Xq, const int8_t *Wq, const float *sW, const float *bp,
+                          int64_t M, int64_t N, int64_t K, uint16_t *Y, int32_t *acc_out,
+                          hipStream_t st) {
+  const unsigned grid = (unsigned)((N + TM * RBW - 1) / (TM * RBW));
+  qgemm_decode2_kernel<TM, MB, RBW, BKD, S, KSW><<<grid, 64 * KSW, 0, st>>>(
+      Xq, Wq, sW, bp, (int)M, (int)N, (int)K, Y, acc_out);
   return hipGetLastError();
 }
 
@@ -551,17 +625,21 @@ using namespace detail;
 hipError_t launch_qgemm(const int8_t *Xq, const int8_t *Wq, const float *sW, const float *bprime,
                         int64_t M, int64_t N, int64_t K, uint16_t *Y, int32_t *acc_out,
                         hipStream_t st) {
-  // Decode: rows per workgroup (16*RB) trade token-row reuse (large RB)
-  // against enough workgroups to fill the GPU (small RB); measured on the
-  // OPT-30B shapes at 1, 8, 32 and 64 tokens.
+  // Decode (M <= 64): weight-streaming ring kernel.  Template arguments
+  // <MFMA rows, token blocks, row blocks per workgroup, BKD, LDS stages, waves
+  // splitting K>, chosen per token count and width from measurements on the
+  // OPT-30B shapes (wide: qkv/fc1; narrow: out/fc2, which need their waves
+  // to split K to keep enough loads in flight).
   const bool wide = N >= 16384;
-  if (M <= 16) return launch_decode<1, 2, 4, 4>(Xq, Wq, sW, bprime, M, N, K, Y, acc_out, st);
+  if (M <= 16)
+    return wide ? launch_decode2<16, 1, 2, 256, 3, 1>(Xq, Wq, sW, bprime, M, N, K, Y, acc_out, st)
+                : launch_decode2<16, 1, 2, 256, 3, 4>(Xq, Wq, sW, bprime, M, N, K, Y, acc_out, st);
   if (M <= 32)
-    return wide ? launch_decode<2, 8, 8, 1>(Xq, Wq, sW, bprime, M, N, K, Y, acc_out, st)
-                : launch_decode<2, 2, 4, 4>(Xq, Wq, sW, bprime, M, N, K, Y, acc_out, st);
+    return wide ? launch_decode2<16, 2, 2, 256, 3, 1>(Xq, Wq, sW, bprime, M, N, K, Y, acc_out, st)
+                : launch_decode2<16, 2, 2, 256, 3, 2>(Xq, Wq, sW, bprime, M, N, K, Y, acc_out, st);
   if (M <= 64)
-    return wide ? launch_decode<4, 4, 8, 1>(Xq, Wq, sW, bprime, M, N, K, Y, acc_out, st)
-                : launch_decode<4, 2, 8, 2>(Xq, Wq, sW, bprime, M, N, K, Y, acc_out, st);
+    return wide ? launch_decode2<16, 4, 4, 256, 4, 1>(Xq, Wq, sW, bprime, M, N, K, Y, acc_out, st)
+                : launch_decode2<16, 4, 2, 256, 3, 2>(Xq, Wq, sW, bprime, M, N, K, Y, acc_out, st);
   return launch_prefill<256, 256, 128, 4, 2, 2>(Xq, Wq, sW, bprime, M, N, K, Y, acc_out, st);
 }
 

@@ -158,6 +158,8 @@ QL_SHAPES = [
     # decode kernel (M <= 64)
     (1, 8, 16), (1, 300, 1040), (5, 772, 768), (16, 256, 4096), (17, 100, 400),
     (32, 513, 128), (33, 64, 48), (64, 1000, 2064),
+    # decode kernel, wide layers (N >= 16384 takes the other configurations)
+    (1, 16400, 272), (9, 16384, 2064), (20, 16448, 528), (64, 16392, 784),
     # prefill kernel
     (65, 256, 128), (200, 300, 400), (256, 256, 256), (300, 772, 1040), (513, 129, 768),
     (600, 1024, 4112),
