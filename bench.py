@@ -47,6 +47,8 @@ def parse():
     p.add_argument("--no-fp16", action="store_true", help="skip the fp16 torch baseline")
     p.add_argument("--no-cpu", action="store_true", help="skip the CPU-oracle baseline")
     p.add_argument("--iters", type=int, default=50, help="iterations for the side measurements")
+    p.add_argument("--copy-probe", action="store_true",
+                   help="only run a plain 1 GiB device copy (calibrates the HBM byte counters)")
     return p.parse_args()
 
 
@@ -139,6 +141,34 @@ def decode_report(torch, ot, synth, wl, pool, iters, with_fp16):
         rec = dict(us_per_stack=med * 1e3, p10_us=p10 * 1e3, p90_us=p90 * 1e3,
                    bytes_per_stack=nbytes, GBps=gbs, frac_of_hbm_peak=gbs / PEAK_HBM_GBS,
                    tokens_per_s=M / (med * 1e-3))
+        # the same stack replayed from a HIP graph (what a decode loop does);
+        # one graph per weight copy, each replay checked against eager
+        ref = [y.clone() for y in ys]
+        graphs = []
+        for c in copies:
+            g = torch.cuda.CUDAGraph()
+            torch.cuda.synchronize()
+            with torch.cuda.graph(g):
+                for i, L in enumerate(c):
+                    ot.ot_qlinear(xq[i], L["Wq"], L["sW"], L["bp"], wl.a_bits, wl.w_bits, ys[i])
+            graphs.append(g)
+        for y in ys:
+            y.zero_()
+        torch.cuda.synchronize()
+        for rep in range(3):
+            graphs[rep & 1].replay()
+            torch.cuda.synchronize()
+            assert all(torch.equal(a, b) for a, b in zip(ys, ref)), "graph replay differs"
+        gi = [0]
+
+        def replay():
+            graphs[gi[0] & 1].replay()
+            gi[0] += 1
+        gmed, _, _ = median_ms(torch, replay, iters)
+        rec["graph_us_per_stack"] = gmed * 1e3
+        rec["graph_GBps"] = nbytes / (gmed * 1e-3) / 1e9
+        rec["graph_frac_of_hbm_peak"] = rec["graph_GBps"] / PEAK_HBM_GBS
+        del graphs
         if with_fp16:
             import torch.nn.functional as F
             w16 = [[L["W16"] for L in layers], [L["W16"].clone() for L in layers]]
@@ -155,8 +185,40 @@ def decode_report(torch, ot, synth, wl, pool, iters, with_fp16):
             rec["speedup_vs_fp16"] = m16 / med
             del w16
         out[str(M)] = rec
-        log(f"decode M={M}: {med * 1e3:.1f} us/stack, {gbs:.0f} GB/s")
+        log(f"decode M={M}: {med * 1e3:.1f} us/stack, {gbs:.0f} GB/s; graph "
+            f"{gmed * 1e3:.1f} us, {rec['graph_GBps']:.0f} GB/s")
     return out
+
+
+def measured_traffic():
+    """HBM bytes per prefill-GEMM launch from the committed counter summary,
+    if it was taken on the current kernel source; else None."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "qgemm_prefill_opt13b_w6a6_traffic.json")
+    src = os.path.join(ROOT, "paper_2406_18832_amd", "csrc", "ot_qgemm.hip")
+    try:
+        with open(path) as f:
+            rec = json.load(f)
+        with open(src, "rb") as f:
+            digest = hashlib.sha256(f.read()).hexdigest()
+    except OSError:
+        return None
+    if rec.get("source_sha256") != digest:
+        return None
+    return rec.get("traffic_bytes_per_launch")
+
+
+def copy_probe(torch):
+    """A plain device copy of exactly 1 GiB (read 1 GiB, write 1 GiB)."""
+    n = 1 << 30
+    a = torch.empty(n, dtype=torch.uint8, device="cuda")
+    a.fill_(1)
+    b = torch.empty_like(a)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_bytes_read": n, "copy_probe_bytes_written": n, "launches": 3}))
 
 
 def cpu_baseline(ot_oracle, layers, M, budget_s=10.0):
@@ -200,6 +262,9 @@ def main():
 
     from paper_2406_18832_amd import ot, synth
     assert torch.cuda.is_available(), "bench.py needs a GPU"
+    if args.copy_probe:
+        copy_probe(torch)
+        return
     ot.lib()
     wl = synth.WORKLOADS[args.workload]
     M = wl.M
@@ -264,7 +329,7 @@ def main():
                    "step": "4 x (ot_quantize_act + ot_qlinear)"},
         "roofline": {"bound": "mfma", "kernel": "qgemm_prefill",
                      "achieved": round(gemm_tops, 2), "peak": PEAK_INT8_TOPS, "unit": "TOP/s",
-                     "frac": round(gemm_tops / PEAK_INT8_TOPS, 4), "traffic": None,
+                     "frac": round(gemm_tops / PEAK_INT8_TOPS, 4), "traffic": measured_traffic(),
                      "ops_per_launch": {L["name"]: 2 * M * L["N"] * L["K"] for L in layers},
                      "ms_per_launch": {L["name"]: round(t, 4) for L, t in zip(layers, per_layer_ms)}},
         "qlinear_tops": round(gemm_tops, 2),
