@@ -49,6 +49,9 @@ def parse():
     p.add_argument("--iters", type=int, default=50, help="iterations for the side measurements")
     p.add_argument("--copy-probe", action="store_true",
                    help="only run a plain 1 GiB device copy (calibrates the HBM byte counters)")
+    p.add_argument("--traffic-record", metavar="DIR",
+                   help="host only: write the prefill GEMM's HBM traffic record from the "
+                        "rocprofv3 counter runs under DIR (fetch/, write/, copy_fetch/, copy_write/)")
     return p.parse_args()
 
 
@@ -190,22 +193,114 @@ def decode_report(torch, ot, synth, wl, pool, iters, with_fp16):
     return out
 
 
+TRAFFIC_RECORD = os.path.join(ROOT, "profiles", "qgemm_prefill_opt13b_w6a6_traffic.json")
+PREFILL_SOURCES = [os.path.join(ROOT, "paper_2406_18832_amd", "csrc", f)
+                   for f in ("ot_prefill.hip", "ot_gemm_common.h")]
+
+
+def prefill_source_digest():
+    import hashlib
+    h = hashlib.sha256()
+    for path in PREFILL_SOURCES:
+        with open(path, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
 def measured_traffic():
     """HBM bytes per prefill-GEMM launch from the committed counter summary,
-    if it was taken on the current kernel source; else None."""
-    import hashlib
-    path = os.path.join(ROOT, "profiles", "qgemm_prefill_opt13b_w6a6_traffic.json")
-    src = os.path.join(ROOT, "paper_2406_18832_amd", "csrc", "ot_qgemm.hip")
+    if it was taken on the current prefill kernel source; else None."""
     try:
-        with open(path) as f:
+        with open(TRAFFIC_RECORD) as f:
             rec = json.load(f)
-        with open(src, "rb") as f:
-            digest = hashlib.sha256(f.read()).hexdigest()
+        digest = prefill_source_digest()
     except OSError:
         return None
     if rec.get("source_sha256") != digest:
         return None
     return rec.get("traffic_bytes_per_launch")
+
+
+def _counter_rows(d, counter):
+    import csv
+    import glob
+    rows = []
+    for path in sorted(glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)):
+        with open(path) as f:
+            rows += [r for r in csv.DictReader(f) if r["Counter_Name"] == counter]
+    if not rows:
+        raise SystemExit(f"no {counter} rows under {d}")
+    return rows
+
+
+def _per_dispatch(rows, name_part):
+    """Counter value summed per dispatch (in dispatch order) for kernels whose
+    name contains name_part, with each dispatch's grid size."""
+    acc, grid = {}, {}
+    for r in rows:
+        if name_part not in r["Kernel_Name"]:
+            continue
+        d = int(r["Dispatch_Id"])
+        acc[d] = acc.get(d, 0.0) + float(r["Counter_Value"])
+        grid[d] = int(r["Grid_Size"])
+    return [(grid[d], acc[d]) for d in sorted(acc)]
+
+
+def traffic_record(d, workload):
+    """Writes the prefill GEMM's HBM traffic record from four rocprofv3 --pmc
+    runs under d: fetch/ and write/ (FETCH_SIZE, WRITE_SIZE of `bench.py
+    --steps 2 --warmup 1 --no-cpu --no-fp16 --no-decode`), copy_fetch/ and
+    copy_write/ (the same counters over `bench.py --copy-probe`).  Host only."""
+    from paper_2406_18832_amd import synth
+    wl = synth.WORKLOADS[workload]
+    n_copy = 1 << 30  # bytes read and written per copy_probe launch
+    factors = {}
+    for c, sub in (("FETCH_SIZE", "copy_fetch"), ("WRITE_SIZE", "copy_write")):
+        disp = _per_dispatch(_counter_rows(os.path.join(d, sub), c), "copyBuffer")
+        kib = [v for _, v in disp if v > 0.5 * n_copy / 1024 / 4]
+        factors[c] = n_copy / 1024 / float(np.median(kib))
+    per = {L.name: {"fetch_kib": [], "write_kib": []} for L in wl.layers}
+    threads = 512  # workgroup size of the prefill kernel (256x256 tiles)
+    for c, sub, key in (("FETCH_SIZE", "fetch", "fetch_kib"), ("WRITE_SIZE", "write", "write_kib")):
+        disp = _per_dispatch(_counter_rows(os.path.join(d, sub), c), "qgemm_prefill_kernel")
+        if len(disp) % len(wl.layers):
+            raise SystemExit(f"{len(disp)} prefill dispatches is not a whole number of steps")
+        for i, (g, v) in enumerate(disp):
+            L = wl.layers[i % len(wl.layers)]
+            tiles = -(-wl.M // 256) * -(-L.N // 256)
+            if g != tiles * threads:
+                raise SystemExit(f"dispatch {i}: grid {g} is not layer {L.name}'s {tiles * threads}")
+            per[L.name][key].append(v)
+    rec_layers, alg = {}, {}
+    for L in wl.layers:
+        f = float(np.mean(per[L.name]["fetch_kib"]))
+        w = float(np.mean(per[L.name]["write_kib"]))
+        rec_layers[L.name] = {"fetch_kib": f, "write_kib": w,
+                              "bytes": (f * factors["FETCH_SIZE"] + w * factors["WRITE_SIZE"]) * 1024}
+        alg[L.name] = wl.M * L.K + L.N * L.K + 2 * wl.M * L.N + 8 * L.N
+    cmd = "cd /tmp && timeout -s KILL 120 rocprofv3 --pmc {c} --output-format csv -d <out>/{sub} -o p -- python -u <repo>/bench.py {args}"
+    bench_args = "--steps 2 --warmup 1 --no-cpu --no-fp16 --no-decode"
+    rec = {
+        "kernel": "qgemm_prefill_kernel<256,256,128,4,2,2,1>",
+        "workload": f"{wl.name} ({wl.M} tokens; " + ", ".join(L.name for L in wl.layers) + ")",
+        "source_files": [os.path.relpath(p, ROOT) for p in PREFILL_SOURCES],
+        "source_sha256": prefill_source_digest(),
+        "copy_factor_fetch": factors["FETCH_SIZE"],
+        "copy_factor_write": factors["WRITE_SIZE"],
+        "per_layer": rec_layers,
+        "algorithmic_bytes_per_layer": alg,
+        "traffic_bytes_per_launch": float(np.mean([v["bytes"] for v in rec_layers.values()])),
+        "algorithmic_bytes_per_launch": float(np.mean(list(alg.values()))),
+        "commands": [cmd.format(c="FETCH_SIZE", sub="fetch", args=bench_args),
+                     cmd.format(c="WRITE_SIZE", sub="write", args=bench_args),
+                     cmd.format(c="FETCH_SIZE", sub="copy_fetch", args="--copy-probe"),
+                     cmd.format(c="WRITE_SIZE", sub="copy_write", args="--copy-probe"),
+                     f"python bench.py --traffic-record <out>"],
+    }
+    with open(TRAFFIC_RECORD, "w") as f:
+        json.dump(rec, f, indent=1)
+    print(json.dumps({k: rec[k] for k in ("traffic_bytes_per_launch", "algorithmic_bytes_per_launch",
+                                          "copy_factor_fetch", "copy_factor_write")}))
 
 
 def copy_probe(torch):
@@ -254,6 +349,9 @@ def cpu_baseline(ot_oracle, layers, M, budget_s=10.0):
 # ---------------------------------------------------------------------------
 def main():
     args = parse()
+    if args.traffic_record:
+        traffic_record(args.traffic_record, args.workload)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the quantized linear "
               "is single-device here and no multi-GPU path is built.", file=sys.stderr)

@@ -1,0 +1,227 @@
+// Decode GEMM of the quantized linear (at most 64 tokens), bound by
+// streaming the weights from HBM.
+#include "ot_gemm_common.h"
+
+namespace ot {
+namespace detail {
+
+// ---------------------------------------------------------------------------
+// Shared-token ring: one LDS ring for tokens and weights
+// ---------------------------------------------------------------------------
+// Loading the token fragments into every wave's registers would limit how
+// far ahead a wave can fetch (and repeat the token loads per wave).  The
+// NW = NR x NK waves of a workgroup step through K together over one ring of
+// S stages.  A stage
+// holds the token tile [16*MB rows][BKD] and the workgroup's weight tile
+// [16*RBW*NR rows][BKD], both filled by buffer load-to-LDS S-1 stages ahead
+// with the loads spread evenly over all waves; one barrier per stage.  Wave
+// (rg, kg) multiplies weight rows 16*RBW*rg.. by every token over the kg-th
+// 1/NK of the stage's 64-byte K steps; the NK partial sums of a row group are
+// added through LDS at the end (integer sums, so the order is immaterial).
+// Chunk c of stage row r sits at chunk c ^ swz_rows(r), which keeps both the
+// fragment reads and the DMA writes free of bank conflicts.
+template <int MB, int NR, int NK, int RBW, int BKD, int S>
+struct DecodeCfg {
+  static constexpr int kWaves = NR * NK;
+  static constexpr int kTokRows = 16 * MB;
+  static constexpr int kWRows = 16 * RBW * NR;
+  static constexpr int kRows = kTokRows + kWRows;
+  static constexpr int kChunks = BKD / 16;
+  static constexpr int kSteps = BKD / 64 / NK;  // 64-byte K steps per wave per stage
+  static constexpr int kStage = kRows * BKD;
+  static constexpr int kRowsPerLoad = 1024 / BKD;
+  static constexpr int kLoads = kStage / 1024 / kWaves;  // per wave per stage
+  static constexpr int kRed = (NK - 1) * NR * RBW * MB * 1024;  // partial sums, bytes
+  static_assert(BKD == 128 || BKD == 256 || BKD == 512, "BKD");
+  static_assert(kSteps >= 1 && kSteps * 64 * NK == BKD, "K steps split evenly over NK");
+  static_assert(kLoads >= 1 && kLoads * 1024 * kWaves == kStage, "stage splits evenly over the waves");
+  static_assert(kTokRows % kRowsPerLoad == 0, "a load never straddles tokens and weights");
+  static_assert((S - 2) * kLoads <= 63 && S >= 2, "vmcnt range");
+  static_assert(kRed <= S * kStage, "partial sums fit in the ring");
+};
+
+template <int kChunks>
+__device__ __forceinline__ int swz_rows(int r) {
+  if constexpr (kChunks == 8) return (r & 7) ^ ((r >> 3) & 1);
+  else return r & 15;
+}
+
+template <int MB, int NR, int NK, int RBW, int BKD, int S>
+__device__ __forceinline__ void decode_body(
+    int8_t *smem, const int8_t *__restrict__ Xq, const int8_t *__restrict__ Wq,
+    const float *__restrict__ sW, const float *__restrict__ bp, int M, int N, int K,
+    uint16_t *__restrict__ Y, int32_t *__restrict__ acc_out) {
+  using C = DecodeCfg<MB, NR, NK, RBW, BKD, S>;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int rg = wave % NR, kg = wave / NR;
+  const int nwg0 = blockIdx.x * C::kWRows;  // first weight row of the workgroup
+  const int rows_w = min(C::kWRows, N - nwg0);
+  const __amdgpu_buffer_rsrc_t rw = make_rsrc(Wq + (int64_t)nwg0 * K, (uint32_t)(rows_w * K));
+  const __amdgpu_buffer_rsrc_t rx = make_rsrc(Xq, (uint32_t)(M * K));
+  const int r16 = lane & 15, c4 = lane >> 4;
+
+  // this wave's j-th load of a stage fills 1 KiB block q = wave*kLoads + j:
+  // stage rows q*kRowsPerLoad.. (tokens below kTokRows, then weights)
+  uint32_t goff[C::kLoads];
+  int gck[C::kLoads];
+#pragma unroll
+  for (int j = 0; j < C::kLoads; ++j) {
+    const int q = wave * C::kLoads + j;
+    const int row = q * C::kRowsPerLoad + lane / C::kChunks;
+    const int ch = (lane % C::kChunks) ^ swz_rows<C::kChunks>(row);
+    gck[j] = ch * 16;
+    const int grow = row < C::kTokRows ? row : row - C::kTokRows;
+    goff[j] = (uint32_t)(grow * K + ch * 16);
+  }
+  const int nst = (K + BKD - 1) / BKD;
+  auto issue = [&](int st) {
+    int8_t *dst = smem + (st % S) * C::kStage;
+    const int k0 = st * BKD;
+#pragma unroll
+    for (int j = 0; j < C::kLoads; ++j) {
+      const int q = wave * C::kLoads + j;  // wave-uniform
+      const uint32_t off = (goff[j] + (uint32_t)k0) | ((uint32_t)(k0 + gck[j] >= K) << 31);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(q * C::kRowsPerLoad < C::kTokRows ? rx : rw,
+                                               (lds_void *)(dst + q * 1024), 16, off, 0, 0, 0);
+    }
+  };
+  // fragment offsets within a stage: lane (r16, c4) of step t reads logical
+  // chunk 4*(kg*kSteps + t) + c4 of weight row (this wave's block i) or
+  // token row (block j)
+  int fragw[C::kSteps][RBW], fragx[C::kSteps][MB];
+#pragma unroll
+  for (int t = 0; t < C::kSteps; ++t) {
+    const int c = 4 * (kg * C::kSteps + t) + c4;
+#pragma unroll
+    for (int i = 0; i < RBW; ++i) {
+      const int row = C::kTokRows + (rg * RBW + i) * 16 + r16;
+      fragw[t][i] = row * BKD + 16 * (c ^ swz_rows<C::kChunks>(row));
+    }
+#pragma unroll
+    for (int j = 0; j < MB; ++j) {
+      const int row = j * 16 + r16;
+      fragx[t][j] = row * BKD + 16 * (c ^ swz_rows<C::kChunks>(row));
+    }
+  }
+
+  v4i acc[RBW][MB];
+#pragma unroll
+  for (int i = 0; i < RBW; ++i)
+#pragma unroll
+    for (int j = 0; j < MB; ++j) acc[i][j] = v4i{};
+
+#pragma unroll
+  for (int t = 0; t < S - 1; ++t) issue(t);
+  wait_vmcnt<(S - 2) * C::kLoads>();
+  lds_barrier();
+  issue(S - 1);
+  for (int st = 0; st < nst; ++st) {
+    const int8_t *src = smem + (st % S) * C::kStage;
+#pragma unroll
+    for (int t = 0; t < C::kSteps; ++t) {
+      v4i wf[RBW], xf[MB];
+#pragma unroll
+      for (int i = 0; i < RBW; ++i) wf[i] = *reinterpret_cast<const v4i *>(src + fragw[t][i]);
+#pragma unroll
+      for (int j = 0; j < MB; ++j) xf[j] = *reinterpret_cast<const v4i *>(src + fragx[t][j]);
+#pragma unroll
+      for (int i = 0; i < RBW; ++i)
+#pragma unroll
+        for (int j = 0; j < MB; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(wf[i], xf[j], acc[i][j], 0, 0, 0);
+    }
+    // stage st+1 has landed once at most S-2 younger stages are in flight;
+    // after the barrier every wave is done with stage st, whose slot takes st+S
+    __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
+    wait_vmcnt<(S - 2) * C::kLoads>();
+    lds_barrier();
+    issue(st + S);
+  }
+  // the ring's last (zero-filling) loads must land before its bytes are reused
+  wait_vmcnt<0>();
+
+  if constexpr (NK > 1) {
+    lds_barrier();
+    v4i *red = reinterpret_cast<v4i *>(smem);
+    if (kg > 0) {
+#pragma unroll
+      for (int i = 0; i < RBW; ++i)
+#pragma unroll
+        for (int j = 0; j < MB; ++j)
+          red[((((kg - 1) * NR + rg) * RBW + i) * MB + j) * 64 + lane] = acc[i][j];
+    }
+    __builtin_amdgcn_s_waitcnt(0xC07F);
+    lds_barrier();
+    if (kg > 0) return;
+#pragma unroll
+    for (int g = 0; g < NK - 1; ++g)
+#pragma unroll
+      for (int i = 0; i < RBW; ++i)
+#pragma unroll
+        for (int j = 0; j < MB; ++j)
+          acc[i][j] += red[(((g * NR + rg) * RBW + i) * MB + j) * 64 + lane];
+  }
+
+  // 16x16 output blocks: lane l holds token l%16 and channels 4*(l/16) + r
+#pragma unroll
+  for (int i = 0; i < RBW; ++i)
+#pragma unroll
+    for (int j = 0; j < MB; ++j) {
+      const int64_t m = j * 16 + r16;
+      const int64_t n = nwg0 + (rg * RBW + i) * 16 + 4 * c4;
+      store4(Y, acc_out, sW, bp, m, n, M, N, acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
+    }
+}
+
+template <int MB, int NR, int NK, int RBW, int BKD, int S>
+__global__ __launch_bounds__(64 * NR * NK) void qgemm_decode_kernel(
+    const int8_t *__restrict__ Xq, const int8_t *__restrict__ Wq, const float *__restrict__ sW,
+    const float *__restrict__ bp, int M, int N, int K, uint16_t *__restrict__ Y,
+    int32_t *__restrict__ acc_out) {
+  __shared__ __attribute__((aligned(1024)))
+  int8_t smem[S * DecodeCfg<MB, NR, NK, RBW, BKD, S>::kStage];
+  decode_body<MB, NR, NK, RBW, BKD, S>(smem, Xq, Wq, sW, bp, M, N, K, Y, acc_out);
+}
+
+template <int MB, int NR, int NK, int RBW, int BKD, int S>
+hipError_t launch_decode(const int8_t *Xq, const int8_t *Wq, const float *sW, const float *bp,
+                          int64_t M, int64_t N, int64_t K, uint16_t *Y, int32_t *acc_out,
+                          hipStream_t st) {
+  constexpr int rows = 16 * RBW * NR;
+  const unsigned grid = (unsigned)((N + rows - 1) / rows);
+  qgemm_decode_kernel<MB, NR, NK, RBW, BKD, S><<<grid, 64 * NR * NK, 0, st>>>(
+      Xq, Wq, sW, bp, (int)M, (int)N, (int)K, Y, acc_out);
+  return hipGetLastError();
+}
+
+}  // namespace detail
+
+using namespace detail;
+
+hipError_t launch_qgemm_decode(const int8_t *Xq, const int8_t *Wq, const float *sW,
+                               const float *bprime, int64_t M, int64_t N, int64_t K,
+                               uint16_t *Y, int32_t *acc_out, hipStream_t st) {
+  // Template arguments
+  // <token blocks, row groups, K groups, row blocks per wave, BKD, stages>.
+  // Up to 16 tokens the workgroup is one 16-row block split over 4 K groups
+  // (small LDS footprint, several workgroups per CU).  For 17-64 tokens a
+  // workgroup of 8 waves fills most of a CU's LDS, so one runs per CU: the
+  // tile height is the smallest of 32/64/128 rows whose grid fits in one
+  // pass over the 256 CUs (taller tiles re-read the token tile less, shorter
+  // ones use more CUs); past 128 rows x 256 CUs, 64-row tiles keep the last
+  // pass's tail short.
+  if (M <= 16) return launch_decode<1, 1, 4, 1, 256, 4>(Xq, Wq, sW, bprime, M, N, K, Y, acc_out, st);
+  constexpr int64_t kCUs = 256;
+  const int rows = N <= 32 * kCUs ? 32 : N <= 64 * kCUs ? 64 : N <= 128 * kCUs ? 128 : 64;
+  if (M <= 32) {
+    if (rows == 32) return launch_decode<2, 2, 4, 1, 256, 4>(Xq, Wq, sW, bprime, M, N, K, Y, acc_out, st);
+    if (rows == 64) return launch_decode<2, 4, 2, 1, 256, 3>(Xq, Wq, sW, bprime, M, N, K, Y, acc_out, st);
+    return launch_decode<2, 4, 2, 2, 256, 3>(Xq, Wq, sW, bprime, M, N, K, Y, acc_out, st);
+  }
+  if (rows == 32) return launch_decode<4, 2, 4, 1, 256, 4>(Xq, Wq, sW, bprime, M, N, K, Y, acc_out, st);
+  if (rows == 64) return launch_decode<4, 4, 2, 1, 256, 3>(Xq, Wq, sW, bprime, M, N, K, Y, acc_out, st);
+  return launch_decode<4, 4, 2, 2, 256, 3>(Xq, Wq, sW, bprime, M, N, K, Y, acc_out, st);
+}
+
+}  // namespace ot

@@ -1,0 +1,354 @@
+// Prefill GEMM of the quantized linear (more than 64 tokens).
+#include "ot_gemm_common.h"
+
+namespace ot {
+namespace detail {
+
+// ---------------------------------------------------------------------------
+// Prefill: LDS-tiled int8 MFMA GEMM (v_mfma_i32_32x32x32_i8)
+// ---------------------------------------------------------------------------
+// Workgroup tile BN (weight rows) x BM (token rows), K tile BK bytes, waves
+// arranged WN x WM, each wave owning a (BN/WN) x (BM/WM) block of 32x32 MFMA
+// tiles, accumulated in the AGPR file.
+//
+// Global -> LDS: buffer "load to LDS" (no registers, no ds_write).  One
+// wave-wide 16-byte-per-lane load fills 1 KiB of LDS, lane i landing at byte
+// 16 i.  LDS holds each operand tile row-major ([rows][BK]) with the 16-byte
+// chunks of each row permuted by swz() so that fragment reads are free of
+// bank conflicts.  The permutation is applied on the global side: each lane
+// fetches the (row, chunk) that belongs at its fixed LDS position.  Buffer loads return
+// zeros past the end of the resource, which pads ragged M and N tiles; a K
+// tail is padded by aiming its lanes at an out-of-range offset.
+//
+// Pipeline: S LDS stages form a ring, K tiles are prefetched S-1 ahead.  Each
+// wave double-buffers its MFMA fragments in registers: while the matrix
+// cores work on one 32-byte K step the fragments of the next are in flight.
+// The one barrier per K tile sits between the last fragment reads of tile t
+// and its last MFMAs; right after it the wave starts reading tile t+1 and
+// refills tile t's stage with tile t+S.
+template <int BN, int BM, int BK, int WN, int WM, int S>
+struct PrefillCfg {
+  static constexpr int kWaves = WN * WM;
+  static constexpr int kThreads = 64 * kWaves;
+  static constexpr int kChunks = BK / 16;         // 16-byte chunks per row
+  static constexpr int kTN = BN / WN, kTM = BM / WM;
+  static constexpr int kFN = kTN / 32, kFM = kTM / 32;
+  static constexpr int kKSteps = BK / 32;
+  static constexpr int kABytes = BN * BK, kBBytes = BM * BK;
+  static constexpr int kStage = kABytes + kBBytes;
+  static constexpr int kLoadsA = kABytes / 1024 / kWaves;
+  static constexpr int kLoadsB = kBBytes / 1024 / kWaves;
+  static constexpr int kLoads = kLoadsA + kLoadsB;  // per wave per K tile
+  static_assert(BK == 64 || BK == 128, "an even number of 32-byte K steps per tile");
+  static_assert(kLoadsA * 1024 * kWaves == kABytes && kLoadsB * 1024 * kWaves == kBBytes,
+                "tile must split evenly into wave loads");
+  static_assert(kTN % 32 == 0 && kTM % 32 == 0, "MFMA tiling");
+  static_assert(S >= 2 && (S - 2) * kLoads <= 63, "vmcnt range");
+  static_assert(S * kStage <= 160 * 1024, "LDS");
+};
+
+// LDS swizzle of an operand tile [rows][BK]: chunk c (16 bytes) of row r is
+// stored at chunk c ^ g(r) of that row.  A fragment read has 16 consecutive
+// rows (lanes) fetch the same logical chunk; with g below those 16 reads
+// cover 16 distinct 16-byte bank groups of a 256-byte window, and any 8 of
+// them (rows 8i..8i+7) cover 8 distinct groups of a 128-byte window, so the
+// read is conflict-free whether the LDS serves 8 or 16 lanes per cycle.
+template <int kChunks>
+__device__ __forceinline__ int swz(int r) {
+  if constexpr (kChunks == 4) return ((r >> 1) & 3) ^ ((r >> 3) & 1);
+  else return (r & 7) ^ ((r >> 3) & 1);
+}
+
+// Scheduling recipe for one K step: DS reads (the next step's fragments) and
+// buffer loads spread one by one between the MFMAs, then the rest of the
+// MFMAs, so the matrix cores never wait on the LDS latency.
+template <int kReads, int kMfma, int kVmem>
+__device__ __forceinline__ void sched_interleave() {
+  constexpr int kMask_MFMA = 0x008, kMask_VMEM_READ = 0x020, kMask_DS_READ = 0x100;
+  constexpr int kPaired = kReads < kMfma ? kReads : kMfma;
+#pragma unroll
+  for (int i = 0; i < kPaired; ++i) {
+    if (i < kVmem) __builtin_amdgcn_sched_group_barrier(kMask_VMEM_READ, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(kMask_DS_READ, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(kMask_MFMA, 1, 0);
+  }
+#pragma unroll
+  for (int i = kPaired; i < kVmem; ++i) __builtin_amdgcn_sched_group_barrier(kMask_VMEM_READ, 1, 0);
+  if (kMfma > kPaired) __builtin_amdgcn_sched_group_barrier(kMask_MFMA, kMfma - kPaired, 0);
+}
+
+// The kernel body lives in a device function: hipcc drops the host stub of a
+// kernel template whose body holds lambdas.
+template <int BN, int BM, int BK, int WN, int WM, int S>
+__device__ __forceinline__ void prefill_body(
+    int8_t *smem, const int8_t *__restrict__ Xq, const int8_t *__restrict__ Wq,
+    const float *__restrict__ sW, const float *__restrict__ bp, int M, int N, int K,
+    uint16_t *__restrict__ Y, int32_t *__restrict__ acc_out, int tiles_m, int tiles_n,
+    int group_m) {
+  using C = PrefillCfg<BN, BM, BK, WN, WM, S>;
+
+  // ---- tile schedule ------------------------------------------------------
+  // The dispatcher deals workgroups to the 8 XCDs round-robin (id mod 8), and
+  // each XCD has its own L2.  Renumber so that each XCD owns a contiguous
+  // range of logical tiles, then walk the tiles in groups of group_m token
+  // tiles so that concurrently running tiles share operand rows in that L2.
+  const int nwg = gridDim.x;
+  const int bid = blockIdx.x;
+  const int xcd = bid & 7, local = bid >> 3;
+  const int per = nwg >> 3, rem = nwg & 7;
+  const int lid = (xcd < rem ? xcd * (per + 1) : rem * (per + 1) + (xcd - rem) * per) + local;
+  const int group_size = group_m * tiles_n;
+  const int first_m = (lid / group_size) * group_m;
+  const int gm = min(tiles_m - first_m, group_m);
+  const int tm = first_m + (lid % group_size) % gm;
+  const int tn = (lid % group_size) / gm;
+  const int n0 = tn * BN, m0 = tm * BM;
+
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int wn = wave % WN, wm = wave / WN;
+
+  // ---- global -> LDS addressing --------------------------------------------
+  const int rows_a = min(BN, N - n0), rows_b = min(BM, M - m0);
+  const __amdgpu_buffer_rsrc_t rsrc_a = make_rsrc(Wq + (int64_t)n0 * K, (uint32_t)(rows_a * K));
+  const __amdgpu_buffer_rsrc_t rsrc_b = make_rsrc(Xq + (int64_t)m0 * K, (uint32_t)(rows_b * K));
+  // Lane i of the j-th 1 KiB load lands at LDS slot 64 j' + i (j' = this
+  // wave's load index in the tile), i.e. row (64 j' + i) / kChunks, physical
+  // chunk i % kChunks; it fetches the logical chunk stored there.
+  constexpr int kRowsPerLoad = 64 / C::kChunks;
+  uint32_t off_a[C::kLoadsA], off_b[C::kLoadsB];
+  int ck_a[C::kLoadsA], ck_b[C::kLoadsB];
+#pragma unroll
+  for (int j = 0; j < C::kLoadsA; ++j) {
+    const int row = (wave * C::kLoadsA + j) * kRowsPerLoad + lane / C::kChunks;
+    ck_a[j] = (lane % C::kChunks) ^ swz<C::kChunks>(row);
+    off_a[j] = (uint32_t)(row * K + ck_a[j] * 16);
+  }
+#pragma unroll
+  for (int j = 0; j < C::kLoadsB; ++j) {
+    const int row = (wave * C::kLoadsB + j) * kRowsPerLoad + lane / C::kChunks;
+    ck_b[j] = (lane % C::kChunks) ^ swz<C::kChunks>(row);
+    off_b[j] = (uint32_t)(row * K + ck_b[j] * 16);
+  }
+  const int KT = (K + BK - 1) / BK;
+
+  auto issue_tile = [&](int kt) {
+    const int k0 = kt * BK;  // every chunk of a tile kt >= KT is out of range
+    int8_t *sa = smem + (kt % S) * C::kStage;
+    int8_t *sb = sa + C::kABytes;
+#pragma unroll
+    for (int j = 0; j < C::kLoadsA; ++j)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          rsrc_a, (lds_void *)(sa + (wave * C::kLoadsA + j) * 1024), 16,
+          k0 + ck_a[j] * 16 < K ? off_a[j] + (uint32_t)k0 : kOobOffset, 0, 0, 0);
+#pragma unroll
+    for (int j = 0; j < C::kLoadsB; ++j)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          rsrc_b, (lds_void *)(sb + (wave * C::kLoadsB + j) * 1024), 16,
+          k0 + ck_b[j] * 16 < K ? off_b[j] + (uint32_t)k0 : kOobOffset, 0, 0, 0);
+  };
+
+  // ---- LDS -> register fragment addressing ----------------------------------
+  // Lane (fr, fh) of a 32x32x32 MFMA reads row fr of a 32-row block, logical
+  // chunk 2s + fh of K step s.  Blocks start at multiples of 32 rows and the
+  // swizzle has period 16, so it depends on fr only.
+  const int fr = lane & 31, fh = lane >> 5;
+  int frag_off[C::kKSteps];
+#pragma unroll
+  for (int s = 0; s < C::kKSteps; ++s)
+    frag_off[s] = fr * BK + 16 * ((2 * s + fh) ^ swz<C::kChunks>(fr));
+  const int a_base = wn * C::kTN * BK;
+  const int b_base = C::kABytes + wm * C::kTM * BK;
+
+  v4i fa[2][C::kFN], fb[2][C::kFM];
+  auto read_frags = [&](int kt, int s, int buf) {
+    const int8_t *st = smem + (kt % S) * C::kStage;
+#pragma unroll
+    for (int f = 0; f < C::kFN; ++f)
+      fa[buf][f] = *reinterpret_cast<const v4i *>(st + a_base + f * 32 * BK + frag_off[s]);
+#pragma unroll
+    for (int g = 0; g < C::kFM; ++g)
+      fb[buf][g] = *reinterpret_cast<const v4i *>(st + b_base + g * 32 * BK + frag_off[s]);
+  };
+
+  v16i acc[C::kFN][C::kFM];
+#pragma unroll
+  for (int f = 0; f < C::kFN; ++f)
+#pragma unroll
+    for (int g = 0; g < C::kFM; ++g) acc[f][g] = v16i{};
+  auto mfmas = [&](int buf) {
+#pragma unroll
+    for (int f = 0; f < C::kFN; ++f)
+#pragma unroll
+      for (int g = 0; g < C::kFM; ++g)
+        acc[f][g] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fa[buf][f], fb[buf][g], acc[f][g], 0, 0, 0);
+  };
+
+  // ---- main loop ----------------------------------------------------------------
+  // Tiles past the end of K are issued too, as out-of-range loads that land
+  // zeros in a stage nobody reads: every iteration then has the same number
+  // of loads in flight and one fixed wait, with no branches in the loop.
+#pragma unroll
+  for (int t = 0; t < S - 1; ++t) issue_tile(t);
+  wait_vmcnt<(S - 2) * C::kLoads>();  // tile 0 has landed
+  lds_barrier();
+  issue_tile(S - 1);
+  read_frags(0, 0, 0);
+
+  for (int kt = 0; kt < KT; ++kt) {
+#pragma unroll
+    for (int s = 0; s + 1 < C::kKSteps; ++s) {
+      read_frags(kt, s + 1, (s + 1) & 1);
+      mfmas(s & 1);
+      // keep the next step's fragment reads spread over this step's MFMAs
+      sched_interleave<C::kFN + C::kFM, C::kFN * C::kFM, 0>();
+    }
+    // This wave's reads of tile kt are complete once lgkmcnt drains; tile
+    // kt+1 has landed once at most S-2 younger tiles (kt+2 .. kt+S-1) are in
+    // flight.  After the barrier every wave is past tile kt, so its stage
+    // takes tile kt+S.  At kt = KT-1 the reads of "tile KT" are unused.
+    // The scheduling fence keeps every MFMA of the steps above ahead of the
+    // wait, so the reads have that long to land.
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
+    wait_vmcnt<(S - 2) * C::kLoads>();
+    lds_barrier();
+    issue_tile(kt + S);
+    read_frags(kt + 1, 0, 0);
+    mfmas(1);
+    sched_interleave<C::kFN + C::kFM, C::kFN * C::kFM, C::kLoads>();
+  }
+  wait_vmcnt<0>();
+
+  // ---- epilogue ----------------------------------------------------------------
+  // 32x32 output block, 16 values per lane: lane l holds column (l mod 32)
+  // and rows 8*(r/4) + 4*(l/32) + (r mod 4) for register r.  Columns are
+  // tokens here and rows are channels, so registers 4j..4j+3 are four
+  // consecutive channels of one token.
+  if (acc_out != nullptr) {  // test path: also stores the raw accumulators
+#pragma unroll
+    for (int f = 0; f < C::kFN; ++f)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int64_t n = n0 + wn * C::kTN + f * 32 + 8 * j + 4 * fh;
+#pragma unroll
+        for (int g = 0; g < C::kFM; ++g) {
+          const int64_t m = m0 + wm * C::kTM + g * 32 + fr;
+          store4(Y, acc_out, sW, bp, m, n, M, N, acc[f][g][4 * j], acc[f][g][4 * j + 1],
+                 acc[f][g][4 * j + 2], acc[f][g][4 * j + 3]);
+        }
+      }
+    return;
+  }
+  // Dequantize into a wave-private fp16 tile [kTM tokens][kTN channels] in
+  // the now idle LDS ring, then write whole token rows with 16-byte stores.
+  // In LDS the 8-byte unit u (4 channels) of token row m sits at unit
+  // u ^ (m mod U), U = kTN/4 units per row (a power of two): the lanes that
+  // write one register group (32 tokens, same channels) then spread over
+  // the banks.
+  constexpr int kUnits = C::kTN / 4;
+  static_assert((kUnits & (kUnits - 1)) == 0 && kUnits >= 16, "row of a power-of-two units");
+  static_assert(C::kWaves * C::kTM * C::kTN * 2 <= S * C::kStage, "epilogue tile fits the ring");
+  __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): this wave's last reads
+  wait_vmcnt<0>();                     // the trailing out-of-range tiles
+  lds_barrier();                        // every wave is done with the ring
+  uint16_t *tile = reinterpret_cast<uint16_t *>(smem) + wave * (C::kTM * C::kTN);
+  const int nw0 = n0 + wn * C::kTN;   // first channel of this wave
+  const int mw0 = m0 + wm * C::kTM;   // first token of this wave
+#pragma unroll
+  for (int f = 0; f < C::kFN; ++f)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int nl = f * 32 + 8 * j + 4 * fh;  // channel within the wave tile
+      const int n = nw0 + nl;
+      float4 s4 = make_float4(0.f, 0.f, 0.f, 0.f), b4 = s4;
+      if (n + 3 < N && (N & 3) == 0) {
+        s4 = *reinterpret_cast<const float4 *>(sW + n);
+        b4 = *reinterpret_cast<const float4 *>(bp + n);
+      } else {
+        if (n + 0 < N) { s4.x = sW[n + 0]; b4.x = bp[n + 0]; }
+        if (n + 1 < N) { s4.y = sW[n + 1]; b4.y = bp[n + 1]; }
+        if (n + 2 < N) { s4.z = sW[n + 2]; b4.z = bp[n + 2]; }
+        if (n + 3 < N) { s4.w = sW[n + 3]; b4.w = bp[n + 3]; }
+      }
+#pragma unroll
+      for (int g = 0; g < C::kFM; ++g) {
+        const int ml = g * 32 + fr;
+        uint2 h;
+        h.x = (uint32_t)dequant(acc[f][g][4 * j + 0], s4.x, b4.x) |
+              ((uint32_t)dequant(acc[f][g][4 * j + 1], s4.y, b4.y) << 16);
+        h.y = (uint32_t)dequant(acc[f][g][4 * j + 2], s4.z, b4.z) |
+              ((uint32_t)dequant(acc[f][g][4 * j + 3], s4.w, b4.w) << 16);
+        const int unit = (nl >> 2) ^ (ml & (kUnits - 1));
+        *reinterpret_cast<uint2 *>(tile + ml * C::kTN + unit * 4) = h;
+      }
+    }
+  __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): the tile is in LDS
+  __builtin_amdgcn_wave_barrier();
+  // Row pass: a lane moves 8 channels (16 bytes); kTN/8 lanes cover a row.
+  constexpr int kLanesPerRow = C::kTN / 8;
+  constexpr int kRowsPerPass = 64 / kLanesPerRow;
+  const int pu = lane % kLanesPerRow;   // 16-byte unit pair in the row
+  const int prow = lane / kLanesPerRow;
+  const bool vec_ok = (N & 7) == 0;
+#pragma unroll 4
+  for (int r0 = 0; r0 < C::kTM; r0 += kRowsPerPass) {
+    const int ml = r0 + prow;
+    const int x = ml & (kUnits - 1);
+    const int pair = pu ^ (x >> 1);
+    uint4 v = *reinterpret_cast<const uint4 *>(tile + ml * C::kTN + pair * 8);
+    if (x & 1) {  // the two 8-byte units of the pair are stored swapped
+      const uint32_t t0 = v.x, t1 = v.y;
+      v.x = v.z; v.y = v.w; v.z = t0; v.w = t1;
+    }
+    const int64_t m = mw0 + ml;
+    const int n = nw0 + pu * 8;
+    if (m < M) {
+      uint16_t *dst = Y + m * (int64_t)N + n;
+      if (vec_ok && n + 7 < N) {
+        *reinterpret_cast<uint4 *>(dst) = v;
+      } else {
+        const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+        for (int i = 0; i < 8; ++i)
+          if (n + i < N) dst[i] = (uint16_t)(w[i >> 1] >> (16 * (i & 1)));
+      }
+    }
+  }
+
+}
+
+template <int BN, int BM, int BK, int WN, int WM, int S, int OCC>
+__global__ __launch_bounds__(64 * WN * WM, OCC) void qgemm_prefill_kernel(
+    const int8_t *__restrict__ Xq, const int8_t *__restrict__ Wq, const float *__restrict__ sW,
+    const float *__restrict__ bp, int M, int N, int K, uint16_t *__restrict__ Y,
+    int32_t *__restrict__ acc_out, int tiles_m, int tiles_n, int group_m) {
+  __shared__ __attribute__((aligned(1024)))
+  int8_t smem[S * PrefillCfg<BN, BM, BK, WN, WM, S>::kStage];
+  prefill_body<BN, BM, BK, WN, WM, S>(smem, Xq, Wq, sW, bp, M, N, K, Y, acc_out, tiles_m,
+                                      tiles_n, group_m);
+}
+
+template <int BN, int BM, int BK, int WN, int WM, int S, int OCC = 1>
+hipError_t launch_prefill(const int8_t *Xq, const int8_t *Wq, const float *sW, const float *bp,
+                          int64_t M, int64_t N, int64_t K, uint16_t *Y, int32_t *acc_out,
+                          hipStream_t st, int group_m = 8) {
+  const int tiles_m = (int)((M + BM - 1) / BM), tiles_n = (int)((N + BN - 1) / BN);
+  const unsigned grid = (unsigned)(tiles_m * tiles_n);
+  qgemm_prefill_kernel<BN, BM, BK, WN, WM, S, OCC><<<grid, 64 * WN * WM, 0, st>>>(
+      Xq, Wq, sW, bp, (int)M, (int)N, (int)K, Y, acc_out, tiles_m, tiles_n, group_m);
+  return hipGetLastError();
+}
+
+}  // namespace detail
+
+using namespace detail;
+
+// One tile shape for every prefill layer: 256x256 output tiles, BK = 128,
+// 8 waves as 4 (weight rows) x 2 (tokens), a 2-stage ring (128 KiB of LDS).
+hipError_t launch_qgemm_prefill(const int8_t *Xq, const int8_t *Wq, const float *sW,
+                                const float *bprime, int64_t M, int64_t N, int64_t K,
+                                uint16_t *Y, int32_t *acc_out, hipStream_t st) {
+  return launch_prefill<256, 256, 128, 4, 2, 2>(Xq, Wq, sW, bprime, M, N, K, Y, acc_out, st);
+}
+
+}  // namespace ot

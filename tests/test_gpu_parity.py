@@ -158,8 +158,12 @@ QL_SHAPES = [
     # decode kernel (M <= 64)
     (1, 8, 16), (1, 300, 1040), (5, 772, 768), (16, 256, 4096), (17, 100, 400),
     (32, 513, 128), (33, 64, 48), (64, 1000, 2064),
-    # decode kernel, wide layers (N >= 16384 takes the other configurations)
+    # decode kernel, every tile height for 17-64 tokens (32 rows up to
+    # N = 8192, 64 rows up to 16384, 128 rows up to 32768, 64 rows beyond),
+    # on both sides of each boundary, with ragged N and K tails
     (1, 16400, 272), (9, 16384, 2064), (20, 16448, 528), (64, 16392, 784),
+    (32, 8192, 512), (48, 8193, 96), (17, 8195, 2000), (33, 12000, 1040),
+    (24, 32768, 160), (40, 32769, 64), (64, 33000, 272), (18, 40003, 48),
     # prefill kernel
     (65, 256, 128), (200, 300, 400), (256, 256, 256), (300, 772, 1040), (513, 129, 768),
     (600, 1024, 4112),
