@@ -28,6 +28,12 @@ int_gemm        Eq. (f) right-hand side: the integer sum over k.
 epilogue        Eq. (g): scale by s^{W_s}_j, then add (z W^T + b).
 qlinear         int_gemm followed by epilogue.
 internal_scaling_fp64   Eq. (d) with unrounded operands (used by the tests).
+layernorm_stats Row mean and variance of the LayerNorm that precedes the
+                linear (Sec. 3.2, Implementation paragraph: quantization
+                fused with the preceding LayerNorm).
+ln_quantize_act LayerNorm with the shift z taken into its bias (Sec. 3.2:
+                z combined with the LayerNorm bias), then Eq. (g)'s
+                per-channel quantization, without an fp16 round trip.
 reference_fp64, folded_fp64     exact-arithmetic references (tests only).
 
 Readings taken where the paper is silent (each applies to both this oracle
@@ -45,8 +51,14 @@ and the HIP path):
     weight scale 1.
   * The compensated bias is kept in float32.
   * Minimum and maximum treat -0 as +0.
+  * LayerNorm statistics (population variance, divisor K) come from exact
+    integer sums of the fp16 inputs scaled by 2^24; mean and variance are
+    then rounded to float64 in the order spelled out in layernorm_stats, and
+    the per-element normalization runs in float32 (see ln_quantize_act).
 """
 from __future__ import annotations
+
+import math
 
 import numpy as np
 
@@ -261,6 +273,80 @@ def internal_scaling_fp64(Xt, Wt, sX, sWvec):
     for k in range(K):
         Y += sX[k] * np.outer(Xt[:, k], Wt[:, k])
     return Y * sWvec[None, :]
+
+
+# --------------------------------------------------------------------------
+# LayerNorm fused with symmetrization and quantization (Sec. 3.2,
+# Implementation paragraph)
+# --------------------------------------------------------------------------
+def layernorm_stats(H):
+    """Mean and population variance (divisor K) of every row of fp16 H [M, K].
+
+    Every fp16 value is an integer multiple of 2^-24, so a_k = h_k * 2^24 is
+    an exact integer (|a_k| < 2^40) and the sums S1 = sum a_k and
+    S2 = sum a_k^2 are taken exactly (Python integers).  Then
+      mean = fl(fl(S1) / K) * 2^-24
+      var  = fl(fl(K * S2 - S1^2) / K^2) * 2^-48
+    where fl() rounds to the nearest float64 (ties to even); K * S2 - S1^2
+    is K^2 times the exact population variance of the a_k.  Returns two
+    float64 arrays [M].
+    """
+    H = np.asarray(H)
+    if H.dtype != np.float16 or H.ndim != 2:
+        raise ValueError("H must be fp16 [M, K]")
+    M, K = H.shape
+    a = H.astype(np.float64) * 2.0 ** 24
+    assert np.all(a == np.trunc(a))
+    a = a.astype(np.int64)
+    mean = np.empty(M)
+    var = np.empty(M)
+    for m in range(M):
+        row = [int(v) for v in a[m]]
+        S1 = sum(row)
+        S2 = sum(v * v for v in row)
+        mean[m] = float(S1) / K * 2.0 ** -24
+        var[m] = float(K * S2 - S1 * S1) / float(K * K) * 2.0 ** -48
+    return mean, var
+
+
+def ln_quantize_act(H, gamma, beta, eps, z, inv_s, a_bits: int):
+    """Codes of the symmetrized LayerNorm output, per input channel.
+
+    The LayerNorm y = (h - mean) / sqrt(var + eps) * gamma + beta is followed
+    by Eq. (g)'s quantization of y - z; with z taken into the LayerNorm's
+    bias (Sec. 3.2) the symmetrized value is produced directly and never
+    stored.  Per row (mean, var from layernorm_stats, eps a float32 value):
+      rstd = 1 / sqrt(var + eps)        float64, each step rounded to nearest
+      mu32, r32 = fp32(mean), fp32(rstd)
+    and per element, every step a float32 operation rounded to nearest even:
+      d = fp32(h) - mu32;  n = d * r32;  g = n * fp32(gamma_k)
+      c = fp32(beta_k) - z_k            (the shifted LayerNorm bias)
+      y = g + c;  u = y * inv_s_k;  q = clip(round(u), -qa, qa)
+    Returns int8 [M, K].
+    """
+    qa = qmax(a_bits)
+    H = np.asarray(H)
+    mean, var = layernorm_stats(H)
+    M, K = H.shape
+    gamma = np.asarray(gamma)
+    beta = np.asarray(beta)
+    if gamma.dtype != np.float16 or beta.dtype != np.float16 or gamma.shape != (K,) \
+            or beta.shape != (K,):
+        raise ValueError("gamma and beta must be fp16 [K]")
+    eps64 = float(np.float32(eps))
+    rstd = np.array([1.0 / math.sqrt(v + eps64) for v in var])
+    mu32 = mean.astype(np.float32)[:, None]
+    r32 = rstd.astype(np.float32)[:, None]
+    z = np.asarray(z, dtype=np.float32)
+    inv_s = np.asarray(inv_s, dtype=np.float32)
+    c = beta.astype(np.float32) - z
+    d = H.astype(np.float32) - mu32
+    n = d * r32
+    g = n * gamma.astype(np.float32)[None, :]
+    y = g + c[None, :]
+    u = y * inv_s[None, :]
+    assert u.dtype == np.float32
+    return np.clip(np.rint(u), -qa, qa).astype(np.int8)
 
 
 def pipeline(X, W, b, calib_batches, a_bits: int, w_bits: int):
