@@ -124,6 +124,36 @@ ot_status ot_quantize_act(const uint16_t *x, int64_t M, int64_t K, int a_bits,
                           void *stream);
 
 /*
+ * ot_ln_quantize_act -- LayerNorm fused with symmetrization and Eq. (g)'s
+ * per-channel quantization (Sec. 3.2: z is taken into the LayerNorm's bias,
+ * Implementation paragraph: the quantization is fused with the LayerNorm
+ * that precedes the linear).  Per row of h, with a_k = h_k * 2^24 (exact
+ * integers), S1 = sum a_k and S2 = sum a_k^2 summed exactly:
+ *   mean = fl64(fl64(S1) / K) * 2^-24
+ *   var  = fl64(fl64(K S2 - S1^2) / K^2) * 2^-48      (divisor K)
+ *   rstd = 1 / sqrt(var + eps)                        (fp64, rounded each step)
+ * and per element, in fp32 rounded to nearest even (no fused multiply-add):
+ *   Xq[m,k] = clip(rne((((h - fp32(mean)) * fp32(rstd)) * gamma_k
+ *                       + (beta_k - z_k)) * inv_s_k), -qa, qa)
+ * The result depends on no summation order, so it is reproducible bit for
+ * bit.  The normalized fp16 activation is never written.
+ *
+ *   h      [M x K] fp16 LayerNorm input (device).  M >= 0 (0 is a no-op),
+ *          16 <= K <= 65536, K % 16 == 0.  Finite values (NaN or infinity
+ *          give unspecified codes for their row).
+ *   gamma, beta  [K] fp16 LayerNorm weight and bias (device).
+ *   eps    the LayerNorm epsilon, finite and >= 0.
+ *   z, inv_s     [K] fp32 from ot_calibrate on the LayerNorm's output.
+ *   Xq     [M x K] int8 output (device).
+ *
+ * Asynchronous on stream.
+ */
+ot_status ot_ln_quantize_act(const uint16_t *h, int64_t M, int64_t K,
+                             const uint16_t *gamma, const uint16_t *beta,
+                             float eps, int a_bits, const float *z,
+                             const float *inv_s, int8_t *Xq, void *stream);
+
+/*
  * ot_qlinear -- the quantized linear: integer GEMM (Eq. (f) right-hand side)
  * with the fused dequantizing epilogue of Eq. (g):
  *   acc[m,n] = sum_k Xq[m,k] Wq[n,k]                       (exact int32)

@@ -13,6 +13,7 @@ namespace {
 // Largest K the kernels' 32-bit in-tile offsets cover (a 256-row tile of
 // K-byte rows must stay below 2^31 bytes).
 constexpr int64_t kMaxK = int64_t(1) << 22;
+constexpr int64_t kMaxLnK = int64_t(1) << 16;  // LayerNorm width (exact sums, one workgroup per row)
 constexpr int64_t kMaxRows = (int64_t(1) << 31) - 1;
 
 bool bits_ok(int bits) { return bits >= 2 && bits <= 8; }
@@ -97,6 +98,20 @@ ot_status ot_quantize_act(const uint16_t *x, int64_t M, int64_t K, int a_bits, c
   if (!aligned16(x) || !aligned16(z) || !aligned16(inv_s) || !aligned16(Xq)) return OT_EINVAL;
   return hip_status(ot::launch_quantize_act(x, M, K, qmax(a_bits), z, inv_s, Xq,
                                             static_cast<hipStream_t>(stream)));
+}
+
+ot_status ot_ln_quantize_act(const uint16_t *h, int64_t M, int64_t K, const uint16_t *gamma,
+                             const uint16_t *beta, float eps, int a_bits, const float *z,
+                             const float *inv_s, int8_t *Xq, void *stream) {
+  if (!bits_ok(a_bits) || M < 0 || K < 0 || !(eps >= 0.f) || eps > 3.4e38f) return OT_EINVAL;
+  if (K < 16 || K % 16 != 0 || K > kMaxLnK || M > kMaxRows) return OT_ESHAPE;
+  if (M == 0) return OT_OK;
+  if (!h || !gamma || !beta || !z || !inv_s || !Xq) return OT_EINVAL;
+  if (!aligned16(h) || !aligned16(gamma) || !aligned16(beta) || !aligned16(z) ||
+      !aligned16(inv_s) || !aligned16(Xq))
+    return OT_EINVAL;
+  return hip_status(ot::launch_ln_quantize_act(h, M, K, gamma, beta, eps, qmax(a_bits), z, inv_s,
+                                               Xq, static_cast<hipStream_t>(stream)));
 }
 
 ot_status ot_qlinear(const int8_t *Xq, const int8_t *Wq, const float *sW, const float *bprime,

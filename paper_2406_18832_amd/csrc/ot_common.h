@@ -46,6 +46,9 @@ hipError_t launch_fold(const uint16_t *W, const uint16_t *b, int64_t N, int64_t 
                        hipStream_t st);
 hipError_t launch_quantize_act(const uint16_t *x, int64_t M, int64_t K, int qa, const float *z,
                                const float *inv_s, int8_t *Xq, hipStream_t st);
+hipError_t launch_ln_quantize_act(const uint16_t *h, int64_t M, int64_t K, const uint16_t *gamma,
+                                  const uint16_t *beta, float eps, int qa, const float *z,
+                                  const float *inv_s, int8_t *Xq, hipStream_t st);
 hipError_t launch_qgemm_decode(const int8_t *Xq, const int8_t *Wq, const float *sW,
                                const float *bprime, int64_t M, int64_t N, int64_t K,
                                uint16_t *Y, int32_t *acc_out, hipStream_t st);

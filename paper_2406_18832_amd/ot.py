@@ -50,6 +50,9 @@ def lib() -> ctypes.CDLL:
         L.ot_fold_weights.argtypes = [vp, vp, i64, i64, c_int, vp, vp, vp, vp, vp, vp]
         L.ot_quantize_act.restype = c_int
         L.ot_quantize_act.argtypes = [vp, i64, i64, c_int, vp, vp, vp, vp]
+        L.ot_ln_quantize_act.restype = c_int
+        L.ot_ln_quantize_act.argtypes = [vp, i64, i64, vp, vp, ctypes.c_float, c_int, vp, vp, vp,
+                                         vp]
         L.ot_qlinear.restype = c_int
         L.ot_qlinear.argtypes = [vp, vp, vp, vp, i64, i64, i64, c_int, c_int, vp, vp, vp, vp]
         L.ot_qlinear_workspace_size.restype = ctypes.c_size_t
@@ -136,6 +139,19 @@ def ot_quantize_act(x, a_bits, z, inv_s, Xq, stream=None):
     _check(rc, "ot_quantize_act")
 
 
+def ot_ln_quantize_act(h, gamma, beta, eps, a_bits, z, inv_s, Xq, stream=None):
+    """h [M, K] fp16 LayerNorm input -> Xq [M, K] int8 codes of the symmetrized
+    LayerNorm output.  Asynchronous."""
+    M, K = h.shape
+    rc = lib().ot_ln_quantize_act(_dev(h, torch.float16, "h"), M, K,
+                                  _dev(gamma, torch.float16, "gamma", (K,)),
+                                  _dev(beta, torch.float16, "beta", (K,)), float(eps), int(a_bits),
+                                  _dev(z, torch.float32, "z", (K,)),
+                                  _dev(inv_s, torch.float32, "inv_s", (K,)),
+                                  _dev(Xq, torch.int8, "Xq", (M, K)), _stream(stream))
+    _check(rc, "ot_ln_quantize_act")
+
+
 def ot_qlinear(Xq, Wq, sW, bprime, a_bits, w_bits, Y, acc_out=None, workspace=None, stream=None):
     """Xq [M, K] int8, Wq [N, K] int8 -> Y [M, N] fp16 (and acc_out [M, N]
     int32 if given).  Asynchronous."""
@@ -192,6 +208,12 @@ def fold_weights(W, b, w_bits, z, s):
 def quantize_act(x, a_bits, z, inv_s):
     Xq = torch.empty(x.shape, dtype=torch.int8, device=x.device)
     ot_quantize_act(x, a_bits, z, inv_s, Xq)
+    return Xq
+
+
+def ln_quantize_act(h, gamma, beta, eps, a_bits, z, inv_s):
+    Xq = torch.empty(h.shape, dtype=torch.int8, device=h.device)
+    ot_ln_quantize_act(h, gamma, beta, eps, a_bits, z, inv_s, Xq)
     return Xq
 
 

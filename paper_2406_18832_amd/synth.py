@@ -29,6 +29,8 @@ ROLE_WEIGHT = 2
 ROLE_BIAS = 3
 ROLE_OUTLIER_SET = 4  # which channels are outliers (fixed per layer)
 ROLE_OFFSETS = 5      # per-channel mean offsets (fixed per layer)
+ROLE_LN_INPUT = 6     # LayerNorm input rows: idx 0 evaluated, 1.. calibration
+ROLE_LN_PARAMS = 7    # LayerNorm gain and bias, and the input's channel moments
 
 
 @dataclass(frozen=True)
@@ -198,3 +200,43 @@ def calibration_batches(wl: Workload, layer_index: int, rows: int | None = None,
     batches = wl.calib_batches if batches is None else batches
     for i in range(batches):
         yield activations(wl, layer_index, rows, ROLE_CALIB_X, i)
+
+
+# --------------------------------------------------------------------------
+# LayerNorm inputs (for the linears that follow a LayerNorm: qkv and fc1)
+# --------------------------------------------------------------------------
+def ln_params(wl: Workload, layer_index: int):
+    """fp16 gamma, beta [K] of the LayerNorm in front of layer ``layer_index``.
+
+    gamma ~ U(0.5, 1.5) and beta ~ N(0, 0.2^2), except on the layer's outlier
+    channels, where gamma ~ U(10, 30) and beta ~ U(-10, 10): the LayerNorm's
+    gain is what turns a few channels into structured outliers of the
+    linear's input, and its bias makes them asymmetric."""
+    K = wl.layers[layer_index].K
+    g = rng(wl, layer_index, ROLE_LN_PARAMS)
+    gamma = g.uniform(0.5, 1.5, size=K)
+    beta = g.normal(0.0, 0.2, size=K)
+    ch = outlier_channels(wl, layer_index, K)
+    gamma[ch] = g.uniform(10.0, 30.0, size=ch.size)
+    beta[ch] = g.uniform(-10.0, 10.0, size=ch.size)
+    return gamma.astype(np.float16), beta.astype(np.float16)
+
+
+def ln_inputs(wl: Workload, layer_index: int, rows: int, idx: int = 0) -> np.ndarray:
+    """fp16 [rows, K] LayerNorm input (the residual stream): per channel k,
+    N(mu_k, sigma_k^2) with sigma_k ~ U(0.5, 2) and mu_k ~ N(0, 0.5^2), the
+    layer's outlier channels with sigma_k = 20 and mu_k ~ U(-40, 40).  The
+    channel moments are fixed per layer; ``idx`` 0 is the evaluated batch,
+    1.. the calibration batches."""
+    K = wl.layers[layer_index].K
+    gp = rng(wl, layer_index, ROLE_LN_PARAMS, 1)
+    sigma = gp.uniform(0.5, 2.0, size=K)
+    mu = gp.normal(0.0, 0.5, size=K)
+    ch = outlier_channels(wl, layer_index, K)
+    sigma[ch] = 20.0
+    mu[ch] = gp.uniform(-40.0, 40.0, size=ch.size)
+    g = rng(wl, layer_index, ROLE_LN_INPUT, idx)
+    x = g.standard_normal(size=(rows, K), dtype=np.float32)
+    x *= sigma.astype(np.float32)[None, :]
+    x += mu.astype(np.float32)[None, :]
+    return x.astype(np.float16)

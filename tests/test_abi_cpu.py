@@ -75,6 +75,21 @@ def test_quantize_act_argument_checks():
     assert L.ot_quantize_act(1, 4, 32, 8, 16, 16, 16, NULL) == ot.OT_EINVAL
 
 
+def test_ln_quantize_act_argument_checks():
+    L = ot.lib()
+    f = L.ot_ln_quantize_act
+    nan = float("nan")
+    assert f(NULL, 4, 24, NULL, NULL, 1e-5, 8, NULL, NULL, NULL, NULL) == ot.OT_ESHAPE
+    assert f(NULL, 4, 65536 + 16, NULL, NULL, 1e-5, 8, NULL, NULL, NULL, NULL) == ot.OT_ESHAPE
+    assert f(NULL, 4, 32, NULL, NULL, 1e-5, 9, NULL, NULL, NULL, NULL) == ot.OT_EINVAL
+    assert f(NULL, 4, 32, NULL, NULL, -1e-5, 8, NULL, NULL, NULL, NULL) == ot.OT_EINVAL
+    assert f(NULL, 4, 32, NULL, NULL, nan, 8, NULL, NULL, NULL, NULL) == ot.OT_EINVAL
+    assert f(NULL, 4, 32, NULL, NULL, float("inf"), 8, NULL, NULL, NULL, NULL) == ot.OT_EINVAL
+    assert f(NULL, 0, 32, NULL, NULL, 1e-5, 8, NULL, NULL, NULL, NULL) == ot.OT_OK
+    assert f(NULL, 4, 32, NULL, NULL, 1e-5, 8, NULL, NULL, NULL, NULL) == ot.OT_EINVAL
+    assert f(16, 4, 32, 16, 16, 1e-5, 8, 16, 16, 8, NULL) == ot.OT_EINVAL  # misaligned Xq
+
+
 def test_calibrate_and_fold_argument_checks():
     L = ot.lib()
     assert L.ot_calibrate(NULL, 4, 32, 8, 1, NULL, NULL, NULL, NULL, NULL) == ot.OT_EINVAL

@@ -1,0 +1,169 @@
+"""GPU parity of ot_ln_quantize_act (LayerNorm fused with symmetrization and
+per-channel quantization, Sec. 3.2) against the CPU oracle, through the C
+ABI: codes are compared bit for bit on every element."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import ot_oracle as O
+from paper_2406_18832_amd import ot, synth
+
+pytestmark = pytest.mark.gpu
+
+
+def case(msg):
+    print(f"[case] {msg}", flush=True)
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def _textbook_ln_fp16(H, gamma, beta, eps):
+    """fp16 LayerNorm output (numpy float64), the data calibration sees."""
+    h = H.astype(np.float64)
+    y = (h - h.mean(1, keepdims=True)) / np.sqrt(h.var(1, keepdims=True) + eps)
+    return (y * gamma.astype(np.float64) + beta.astype(np.float64)).astype(np.float16)
+
+
+def _random_inputs(M, K, seed, a_bits=8, eps=1e-5):
+    r = np.random.default_rng(seed)
+    sigma = r.uniform(0.3, 3.0, K)
+    mu = r.normal(0, 2.0, K)
+    out = r.choice(K, size=max(1, K // 100), replace=False)
+    sigma[out] *= 20
+    H = (r.standard_normal((M, K)) * sigma + mu).astype(np.float16)
+    gamma = r.uniform(0.5, 1.5, K)
+    gamma[out] = r.uniform(5, 20, out.size)
+    gamma = gamma.astype(np.float16)
+    beta = r.normal(0, 0.5, K).astype(np.float16)
+    calib = (r.standard_normal((64, K)) * sigma + mu).astype(np.float16)
+    _, z, s, inv_s = O.calibrate([_textbook_ln_fp16(calib, gamma, beta, eps)], a_bits)
+    return H, gamma, beta, z, inv_s
+
+
+def _run(H, gamma, beta, eps, a_bits, z, inv_s):
+    Xq = ot.ln_quantize_act(dev(H), dev(gamma), dev(beta), eps, a_bits, dev(z), dev(inv_s))
+    torch.cuda.synchronize()
+    return Xq.cpu().numpy()
+
+
+# widths on both sides of the 16384 / 32768 kernel-configuration boundaries,
+# ragged against the 8-channel chunks and the 64-thread waves
+SHAPES = [(1, 16), (3, 768), (17, 1040), (130, 512), (64, 4096), (9, 5120), (5, 16384),
+          (2, 16400), (3, 32768), (2, 32784), (1, 65536)]
+
+
+@pytest.mark.parametrize("M,K", SHAPES)
+def test_parity_random(M, K):
+    case(f"ln_quantize M={M} K={K}")
+    H, gamma, beta, z, inv_s = _random_inputs(M, K, 100 * M + K)
+    got = _run(H, gamma, beta, 1e-5, 8, z, inv_s)
+    ref = O.ln_quantize_act(H, gamma, beta, 1e-5, z, inv_s, 8)
+    assert np.array_equal(got, ref)
+
+
+@pytest.mark.parametrize("a_bits", [6, 4, 2])
+def test_parity_low_bits(a_bits):
+    case(f"ln_quantize a_bits={a_bits}")
+    H, gamma, beta, z, inv_s = _random_inputs(40, 2064, 7 + a_bits, a_bits)
+    got = _run(H, gamma, beta, 1e-5, a_bits, z, inv_s)
+    ref = O.ln_quantize_act(H, gamma, beta, 1e-5, z, inv_s, a_bits)
+    assert np.array_equal(got, ref)
+    assert np.abs(got).max() <= O.qmax(a_bits)
+
+
+def test_parity_extreme_rows():
+    """Largest fp16 magnitudes (128-bit sums with a high word), subnormals,
+    zero and constant rows, a single spike, alternating extremes."""
+    case("ln_quantize extreme rows")
+    K = 1024
+    r = np.random.default_rng(3)
+    rows = [
+        np.full(K, 65504.0), np.full(K, -65504.0),
+        np.where(np.arange(K) % 2 == 0, 65504.0, -65504.0),
+        np.zeros(K), np.full(K, 3.0),
+        r.integers(-1023, 1024, K) * 2.0 ** -24,  # subnormals only
+        np.concatenate([[60000.0], np.full(K - 1, 2.0 ** -24)]),
+        np.clip(r.standard_normal(K) * 20000.0, -65504.0, 65504.0),
+        np.where(r.random(K) < 0.5, 6.0e-8, 65000.0),
+    ]
+    H = np.stack(rows).astype(np.float16)
+    assert np.all(np.isfinite(H.astype(np.float32)))
+    gamma = r.uniform(0.5, 1.5, K).astype(np.float16)
+    beta = r.normal(0, 1, K).astype(np.float16)
+    z = r.normal(0, 0.5, K).astype(np.float32)
+    inv_s = r.uniform(10, 40, K).astype(np.float32)
+    for eps in (1e-5, 1e-12, 1.0):
+        got = _run(H, gamma, beta, eps, 8, z, inv_s)
+        ref = O.ln_quantize_act(H, gamma, beta, eps, z, inv_s, 8)
+        assert np.array_equal(got, ref), f"eps={eps}"
+
+
+def test_eps_zero_on_rows_with_spread():
+    case("ln_quantize eps=0")
+    H, gamma, beta, z, inv_s = _random_inputs(16, 768, 21)
+    assert np.array_equal(_run(H, gamma, beta, 0.0, 8, z, inv_s),
+                          O.ln_quantize_act(H, gamma, beta, 0.0, z, inv_s, 8))
+
+
+@pytest.mark.parametrize("name,li", [("opt125m_w8a8", 0), ("opt6.7b_w8a8", 2),
+                                     ("opt13b_w6a6", 0), ("opt66b_w8a8", 0)])
+def test_parity_workload_inputs(name, li):
+    """The seeded LayerNorm inputs of the workloads, calibrated on the fp16
+    LayerNorm output of their calibration rows."""
+    wl = synth.WORKLOADS[name]
+    K = wl.layers[li].K
+    case(f"ln_quantize {name}/{wl.layers[li].name} K={K}")
+    gamma, beta = synth.ln_params(wl, li)
+    calib = [_textbook_ln_fp16(synth.ln_inputs(wl, li, 128, 1 + i), gamma, beta, 1e-5)
+             for i in range(2)]
+    _, z, s, inv_s = O.calibrate(calib, wl.a_bits)
+    H = synth.ln_inputs(wl, li, 24)
+    got = _run(H, gamma, beta, 1e-5, wl.a_bits, z, inv_s)
+    assert np.array_equal(got, O.ln_quantize_act(H, gamma, beta, 1e-5, z, inv_s, wl.a_bits))
+
+
+def test_fullsize_opt13b_qkv_input_sampled_rows():
+    """4096 x 5120 (the OPT-13B qkv input): every code in range, sampled rows
+    against the oracle, and the run repeated gives identical bytes."""
+    wl = synth.WORKLOADS["opt13b_w6a6"]
+    K, M = wl.layers[0].K, wl.M
+    case(f"ln_quantize fullsize M={M} K={K}")
+    gamma, beta = synth.ln_params(wl, 0)
+    calib = [_textbook_ln_fp16(synth.ln_inputs(wl, 0, 256, 1), gamma, beta, 1e-5)]
+    _, z, s, inv_s = O.calibrate(calib, wl.a_bits)
+    H = synth.ln_inputs(wl, 0, M)
+    args = (dev(H), dev(gamma), dev(beta), 1e-5, wl.a_bits, dev(z), dev(inv_s))
+    Xq = ot.ln_quantize_act(*args)
+    Xq2 = ot.ln_quantize_act(*args)
+    torch.cuda.synchronize()
+    assert torch.equal(Xq, Xq2)
+    assert int(Xq.abs().max()) <= O.qmax(wl.a_bits)
+    rows = np.array(sorted(set(np.random.default_rng(1).choice(M, 48, replace=False).tolist())
+                           | {0, M - 1}))
+    got = Xq.index_select(0, torch.from_numpy(rows).cuda()).cpu().numpy()
+    assert np.array_equal(got, O.ln_quantize_act(H[rows], gamma, beta, 1e-5, z, inv_s, wl.a_bits))
+
+
+def test_close_to_unfused_layernorm_then_quantize():
+    """Fused codes against torch's fp32 LayerNorm rounded to fp16 followed by
+    ot_quantize_act: the fused path skips that fp16 rounding, so codes may
+    differ by one where the fp16 rounding crosses a rounding boundary."""
+    case("ln_quantize vs unfused")
+    H, gamma, beta, z, inv_s = _random_inputs(256, 2048, 5)
+    got = _run(H, gamma, beta, 1e-5, 8, z, inv_s)
+    h = dev(H)
+    X = torch.nn.functional.layer_norm(h.float(), (2048,), dev(gamma).float(), dev(beta).float(),
+                                       1e-5).half()
+    unfused = ot.quantize_act(X, 8, dev(z), dev(inv_s)).cpu().numpy()
+    d = np.abs(got.astype(int) - unfused)
+    assert d.max() <= 1 and (d > 0).mean() < 0.1
+
+
+def test_rejects_too_wide_rows():
+    h = torch.zeros((2, 65536 + 16), dtype=torch.float16, device="cuda")
+    p = torch.zeros(65536 + 16, dtype=torch.float16, device="cuda")
+    f = torch.zeros(65536 + 16, dtype=torch.float32, device="cuda")
+    with pytest.raises(ot.OTError):
+        ot.ln_quantize_act(h, p, p, 1e-5, 8, f, f)
