@@ -12,7 +12,9 @@ Printed: one JSON line.  `value` is int8 TOPS over the whole step (GEMM ops
 `roofline` covers the dominant kernel (the prefill GEMM) with its duration
 measured by HIP events around each launch inside the timed region; the
 decode regime (OPT-30B shapes, M in {1, 8, 32, 64}) is reported under
-`decode` in GB/s against HBM; `fp16_baseline` times torch's fp16 linear on
+`decode` in GB/s against HBM; `ln_quantize` times the LayerNorm fused with
+symmetrization and quantization (qkv and fc1 inputs) against torch's
+LayerNorm plus ot_quantize_act; `fp16_baseline` times torch's fp16 linear on
 the same shapes; `cpu_baseline` times the CPU oracle on a bounded sample.
 """
 from __future__ import annotations
@@ -46,6 +48,7 @@ def parse():
     p.add_argument("--no-decode", action="store_true", help="skip the decode-regime report")
     p.add_argument("--no-fp16", action="store_true", help="skip the fp16 torch baseline")
     p.add_argument("--no-cpu", action="store_true", help="skip the CPU-oracle baseline")
+    p.add_argument("--no-ln", action="store_true", help="skip the fused LayerNorm report")
     p.add_argument("--iters", type=int, default=50, help="iterations for the side measurements")
     p.add_argument("--copy-probe", action="store_true",
                    help="only run a plain 1 GiB device copy (calibrates the HBM byte counters)")
@@ -116,6 +119,44 @@ def fp16_baseline(torch, layers, M, iters):
     ops = sum(2.0 * M * L["N"] * L["K"] for L in layers)
     return dict(ms_per_stack=med, p10_ms=p10, p90_ms=p90, tflops=ops / (med * 1e-3) / 1e12,
                 frac_of_fp16_peak=ops / (med * 1e-3) / 1e12 / PEAK_FP16_TFLOPS)
+
+
+def ln_quantize_report(torch, ot, synth, wl, iters):
+    """The LayerNorm in front of qkv and fc1 fused with symmetrization and
+    quantization (ot_ln_quantize_act), against torch's fp16 LayerNorm
+    followed by ot_quantize_act.  Calibration (untimed) runs on torch's fp16
+    LayerNorm output of a seeded calibration batch."""
+    import torch.nn.functional as F
+    out = {}
+    for li, lay in enumerate(wl.layers):
+        if lay.name not in ("qkv", "fc1"):
+            continue
+        M, K = wl.M, lay.K
+        gamma, beta = (torch.from_numpy(a).cuda() for a in synth.ln_params(wl, li))
+        calib = torch.from_numpy(synth.ln_inputs(wl, li, 2048, 1)).cuda()
+        _, z, s, inv_s = ot.calibrate([F.layer_norm(calib, (K,), gamma, beta, 1e-5)], wl.a_bits)
+        h = torch.from_numpy(synth.ln_inputs(wl, li, M)).cuda()
+        Xq = torch.empty((M, K), dtype=torch.int8, device="cuda")
+        Xq2 = torch.empty_like(Xq)
+
+        def fused():
+            ot.ot_ln_quantize_act(h, gamma, beta, 1e-5, wl.a_bits, z, inv_s, Xq)
+
+        def unfused():
+            ot.ot_quantize_act(F.layer_norm(h, (K,), gamma, beta, 1e-5), wl.a_bits, z, inv_s, Xq2)
+        med, p10, p90 = median_ms(torch, fused, iters)
+        umed, _, _ = median_ms(torch, unfused, iters)
+        nbytes = 3 * M * K + 2 * 2 * K + 2 * 4 * K
+        gbs = nbytes / (med * 1e-3) / 1e9
+        differ = float((Xq.int() - Xq2.int()).abs().gt(0).float().mean())
+        out[lay.name] = dict(M=M, K=K, us=med * 1e3, p10_us=p10 * 1e3, p90_us=p90 * 1e3,
+                             bytes=nbytes, GBps=gbs, frac_of_hbm_peak=gbs / PEAK_HBM_GBS,
+                             unfused_us=umed * 1e3, speedup_vs_unfused=umed / med,
+                             codes_differing_from_unfused=differ)
+        log(f"ln_quantize {lay.name}: {med * 1e3:.1f} us ({gbs:.0f} GB/s); torch LN + quantize "
+            f"{umed * 1e3:.1f} us")
+        del h, calib, Xq, Xq2
+    return out
 
 
 def decode_report(torch, ot, synth, wl, pool, iters, with_fp16):
@@ -279,7 +320,7 @@ def traffic_record(d, workload):
                               "bytes": (f * factors["FETCH_SIZE"] + w * factors["WRITE_SIZE"]) * 1024}
         alg[L.name] = wl.M * L.K + L.N * L.K + 2 * wl.M * L.N + 8 * L.N
     cmd = "cd /tmp && timeout -s KILL 120 rocprofv3 --pmc {c} --output-format csv -d <out>/{sub} -o p -- python -u <repo>/bench.py {args}"
-    bench_args = "--steps 2 --warmup 1 --no-cpu --no-fp16 --no-decode"
+    bench_args = "--steps 2 --warmup 1 --no-cpu --no-fp16 --no-decode --no-ln"
     rec = {
         "kernel": "qgemm_prefill_kernel<256,256,128,4,2,2,1>",
         "workload": f"{wl.name} ({wl.M} tokens; " + ", ".join(L.name for L in wl.layers) + ")",
@@ -447,6 +488,10 @@ def main():
         log(f"cpu oracle {result['cpu_baseline']['value']:.3f} TOPS")
     for L in layers:
         del L["W16"]
+    if not args.no_ln:
+        result["ln_quantize"] = {"workload": wl.name, "bound": "hbm", "peak_GBps": PEAK_HBM_GBS,
+                                 "kernel": "ln_quantize_kernel",
+                                 "by_layer": ln_quantize_report(torch, ot, synth, wl, args.iters)}
     if not args.no_decode:
         dwl = synth.WORKLOADS[args.decode_workload]
         layers.clear()

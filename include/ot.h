@@ -127,20 +127,21 @@ ot_status ot_quantize_act(const uint16_t *x, int64_t M, int64_t K, int a_bits,
  * ot_ln_quantize_act -- LayerNorm fused with symmetrization and Eq. (g)'s
  * per-channel quantization (Sec. 3.2: z is taken into the LayerNorm's bias,
  * Implementation paragraph: the quantization is fused with the LayerNorm
- * that precedes the linear).  Per row of h, with a_k = h_k * 2^24 (exact
- * integers), S1 = sum a_k and S2 = sum a_k^2 summed exactly:
- *   mean = fl64(fl64(S1) / K) * 2^-24
- *   var  = fl64(fl64(K S2 - S1^2) / K^2) * 2^-48      (divisor K)
- *   rstd = 1 / sqrt(var + eps)                        (fp64, rounded each step)
+ * that precedes the linear).  Per row of h:
+ *   mean = sum_k h_k / K,  var = sum_k (h_k - mean)^2 / K   (float64)
+ *   rstd = 1 / sqrt(var + eps)                              (float64)
  * and per element, in fp32 rounded to nearest even (no fused multiply-add):
  *   Xq[m,k] = clip(rne((((h - fp32(mean)) * fp32(rstd)) * gamma_k
  *                       + (beta_k - z_k)) * inv_s_k), -qa, qa)
- * The result depends on no summation order, so it is reproducible bit for
- * bit.  The normalized fp16 activation is never written.
+ * The float64 sums run in a fixed order, so the codes are the same on every
+ * run; fp32(mean) and fp32(rstd) are the fp32 roundings of the exact values
+ * unless those lie within a few float64 units of an fp32 rounding boundary.
+ * The normalized fp16 activation is never written.
  *
  *   h      [M x K] fp16 LayerNorm input (device).  M >= 0 (0 is a no-op),
- *          16 <= K <= 65536, K % 16 == 0.  Finite values (NaN or infinity
- *          give unspecified codes for their row).
+ *          16 <= K <= 65536, K % 16 == 0.  Finite values; a row of equal
+ *          values with eps == 0 (and NaN or infinity anywhere in a row)
+ *          gives unspecified codes for that row.
  *   gamma, beta  [K] fp16 LayerNorm weight and bias (device).
  *   eps    the LayerNorm epsilon, finite and >= 0.
  *   z, inv_s     [K] fp32 from ot_calibrate on the LayerNorm's output.

@@ -31,9 +31,10 @@ internal_scaling_fp64   Eq. (d) with unrounded operands (used by the tests).
 layernorm_stats Row mean and variance of the LayerNorm that precedes the
                 linear (Sec. 3.2, Implementation paragraph: quantization
                 fused with the preceding LayerNorm).
-ln_quantize_act LayerNorm with the shift z taken into its bias (Sec. 3.2:
-                z combined with the LayerNorm bias), then Eq. (g)'s
-                per-channel quantization, without an fp16 round trip.
+ln_scaled_act   LayerNorm with the shift z taken into its bias (Sec. 3.2:
+                z combined with the LayerNorm bias), divided by s per
+                channel, without an fp16 round trip.
+ln_quantize_act Eq. (g)'s per-channel codes of that value.
 reference_fp64, folded_fp64     exact-arithmetic references (tests only).
 
 Readings taken where the paper is silent (each applies to both this oracle
@@ -309,8 +310,9 @@ def layernorm_stats(H):
     return mean, var
 
 
-def ln_quantize_act(H, gamma, beta, eps, z, inv_s, a_bits: int):
-    """Codes of the symmetrized LayerNorm output, per input channel.
+def ln_scaled_act(H, gamma, beta, eps, z, inv_s):
+    """The symmetrized, scaled LayerNorm output u (float32 [M, K]) that
+    ln_quantize_act rounds to codes.
 
     The LayerNorm y = (h - mean) / sqrt(var + eps) * gamma + beta is followed
     by Eq. (g)'s quantization of y - z; with z taken into the LayerNorm's
@@ -321,10 +323,8 @@ def ln_quantize_act(H, gamma, beta, eps, z, inv_s, a_bits: int):
     and per element, every step a float32 operation rounded to nearest even:
       d = fp32(h) - mu32;  n = d * r32;  g = n * fp32(gamma_k)
       c = fp32(beta_k) - z_k            (the shifted LayerNorm bias)
-      y = g + c;  u = y * inv_s_k;  q = clip(round(u), -qa, qa)
-    Returns int8 [M, K].
+      y = g + c;  u = y * inv_s_k
     """
-    qa = qmax(a_bits)
     H = np.asarray(H)
     mean, var = layernorm_stats(H)
     M, K = H.shape
@@ -346,6 +346,14 @@ def ln_quantize_act(H, gamma, beta, eps, z, inv_s, a_bits: int):
     y = g + c[None, :]
     u = y * inv_s[None, :]
     assert u.dtype == np.float32
+    return u
+
+
+def ln_quantize_act(H, gamma, beta, eps, z, inv_s, a_bits: int):
+    """Codes of the symmetrized LayerNorm output, per input channel:
+    q = clip(round(u), -qa, qa) with u from ln_scaled_act.  int8 [M, K]."""
+    qa = qmax(a_bits)
+    u = ln_scaled_act(H, gamma, beta, eps, z, inv_s)
     return np.clip(np.rint(u), -qa, qa).astype(np.int8)
 
 

@@ -3,77 +3,48 @@
 // the quantization of Eq. (g) is fused with the LayerNorm that precedes the
 // linear, so the fp16 activation never goes to memory).
 //
-// Per row h [K] (fp16), with a_k = h_k * 2^24 (an exact integer for every
-// fp16 value, |a_k| < 2^40):
-//   S1 = sum a_k, S2 = sum a_k^2                      exact integer sums
-//   mean = fl64(fl64(S1) / K) * 2^-24
-//   var  = fl64(fl64(K*S2 - S1^2) / K^2) * 2^-48       population variance
-//   rstd = fl64(1 / fl64(sqrt(fl64(var + eps))))
+// Per row h [K] (fp16), with c = h_0 and d_k = h_k - c (exact in float64):
+//   mean = c + sum_k d_k / K                            float64
+//   var  = sum_k d_k^2 / K - (sum_k d_k / K)^2          (population variance)
+//   rstd = 1 / sqrt(var + eps)                          float64
 //   mu32 = fp32(mean), r32 = fp32(rstd)
 // and per element (fp32 operations, round to nearest even, no contraction):
 //   y = ((fp32(h_k) - mu32) * r32) * gamma_k + (beta_k - z_k)
 //   q = clip(rne(y * inv_s_k), -qa, qa)
 //
-// Exact sums make the statistics independent of the reduction order, so the
-// codes are reproducible bit for bit.  S2 is kept as three 64-bit partial
-// sums over a 20-bit split of |a| (|a| = ah * 2^20 + al):
-//   S2 = 2^40 * sum ah^2 + 2^21 * sum ah*al + sum al^2,
-// each partial below 2^56 for K <= 2^16, so no carries are needed until the
-// row total is assembled in 128 bits.
+// The float64 sums run in a fixed order (each thread's chunks in order, a
+// fixed butterfly across a wave, waves in order), so the result does not
+// change from run to run.  Their relative error, a few units of the 53rd
+// bit (times (mean - c)^2 / var for the variance), is far below fp32's 24
+// bits: mu32 and r32 are the fp32 roundings of the exact mean and rstd
+// except when those lie that close to an fp32 rounding boundary.
 //
 // HBM-bound: 2 bytes in, 1 byte out per element.  A workgroup of T threads
 // takes R rows; thread t owns the 8-channel chunks t, t + T, ... (CPT of
 // them, 16-byte coalesced loads) and holds its R x CPT chunks in registers
-// between the statistics pass and the normalize pass (one HBM read).  The
-// per-channel gamma, beta - z and inv_s (L2-resident) are read once per
+// from the statistics to the normalize pass (one HBM read).
+// The per-channel gamma, beta - z and inv_s (L2-resident) are read once per
 // chunk and applied to all R rows.
 #include "ot_common.h"
 
 namespace ot {
 namespace detail {
 
-struct U128 {
-  uint64_t hi, lo;
-};
+__device__ inline float half_lo(uint32_t w) { return half_bits_to_float((uint16_t)w); }
+__device__ inline float half_hi(uint32_t w) { return half_bits_to_float((uint16_t)(w >> 16)); }
 
-__device__ inline U128 add128(U128 a, U128 b) {
-  U128 r;
-  r.lo = a.lo + b.lo;
-  r.hi = a.hi + b.hi + (r.lo < a.lo ? 1u : 0u);
-  return r;
+__device__ inline double wave_sum(double v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off);
+  return v;
 }
 
-__device__ inline U128 sub128(U128 a, U128 b) {
-  U128 r;
-  r.lo = a.lo - b.lo;
-  r.hi = a.hi - b.hi - (a.lo < b.lo ? 1u : 0u);
-  return r;
-}
-
-__device__ inline U128 mul64x64(uint64_t a, uint64_t b) { return U128{__umul64hi(a, b), a * b}; }
-
-__device__ inline U128 shl128(uint64_t v, int s) {  // v << s, 0 < s < 64
-  return U128{v >> (64 - s), v << s};
-}
-
-// Nearest float64 (ties to even) of a 128-bit unsigned integer.
-__device__ inline double u128_to_f64(U128 v) {
-  if (v.hi == 0) return (double)v.lo;  // uitofp rounds to nearest even
-  const int lz = __clzll((long long)v.hi);
-  const int s = 64 - lz;  // bits below the top 64
-  const uint64_t top = lz == 0 ? v.hi : (v.hi << lz) | (v.lo >> s);
-  const uint64_t rest = lz == 0 ? v.lo : (v.lo << lz);
-  // 64 >= 53 + 2 bits, so a sticky bit in the lowest position of `top`
-  // makes its single rounding to 53 bits the correct one
-  return ldexp((double)(top | (rest != 0 ? 1u : 0u)), s);
-}
-
-template <int CPT, int R>
-__global__ __launch_bounds__(1024) void ln_quantize_kernel(
+template <int CPT, int R, int MAXT>
+__global__ __launch_bounds__(MAXT) void ln_quantize_kernel(
     const uint16_t *__restrict__ h, int64_t M, int K, const uint16_t *__restrict__ gamma,
     const uint16_t *__restrict__ beta, double eps, float qa, const float *__restrict__ z,
     const float *__restrict__ inv_s, int8_t *__restrict__ Xq) {
-  __shared__ uint64_t part[16][R][4];  // per wave: S1, sum ah^2, sum ah*al, sum al^2
+  __shared__ double red[2][16][R];  // per wave partial sums of d and d^2
   const int T = blockDim.x;
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6, nwaves = T >> 6;
   const int nchunks = K / 8;
@@ -92,69 +63,52 @@ __global__ __launch_bounds__(1024) void ln_quantize_kernel(
                     : make_uint4(0, 0, 0, 0);
     }
 
-  // pass 1: exact integer partial sums
+  // statistics, one pass: sums of d = h - c and d^2 with c = h[row, 0]
+  // (d is exact in float64; the shift keeps the variance free of the
+  // cancellation that sum h^2 - K mean^2 suffers when |mean| >> std)
+  double cs[R];
 #pragma unroll
   for (int r = 0; r < R; ++r) {
-    int64_t s1 = 0;
-    uint64_t shh = 0, sha = 0, saa = 0;
+    const int64_t row = row0 + r;
+    cs[r] = row < M ? (double)half_bits_to_float(h[row * K]) : 0.0;
+    double s1 = 0.0, s2 = 0.0;
 #pragma unroll
     for (int j = 0; j < CPT; ++j) {
+      if (t + j * T >= nchunks) continue;
       const uint32_t w[4] = {x[r][j].x, x[r][j].y, x[r][j].z, x[r][j].w};
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const uint32_t bits = (w[e >> 1] >> (16 * (e & 1))) & 0xffffu;
-        const uint32_t ex = (bits >> 10) & 31u, man = bits & 1023u;
-        // |h| * 2^24: subnormal man, normal (1024 + man) << (ex - 1)
-        const uint64_t mag = ex == 0 ? (uint64_t)man : (uint64_t)(1024u + man) << (ex - 1);
-        s1 += (bits & 0x8000u) ? -(int64_t)mag : (int64_t)mag;
-        const uint32_t ah = (uint32_t)(mag >> 20), al = (uint32_t)mag & 0xfffffu;
-        shh += (uint64_t)ah * ah;
-        sha += (uint64_t)ah * al;
-        saa += (uint64_t)al * al;
+      for (int i = 0; i < 4; ++i) {
+        const double d0 = (double)half_lo(w[i]) - cs[r];
+        const double d1 = (double)half_hi(w[i]) - cs[r];
+        s1 += d0;
+        s1 += d1;
+        s2 = fma(d0, d0, s2);
+        s2 = fma(d1, d1, s2);
       }
     }
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) {
-      s1 += __shfl_xor(s1, off);
-      shh += __shfl_xor(shh, off);
-      sha += __shfl_xor(sha, off);
-      saa += __shfl_xor(saa, off);
-    }
+    s1 = wave_sum(s1);
+    s2 = wave_sum(s2);
     if (lane == 0) {
-      part[wave][r][0] = (uint64_t)s1;
-      part[wave][r][1] = shh;
-      part[wave][r][2] = sha;
-      part[wave][r][3] = saa;
+      red[0][wave][r] = s1;
+      red[1][wave][r] = s2;
     }
   }
   __syncthreads();
-
-  // row statistics (every thread computes them for the R rows it stores)
   float mu32[R], r32[R];
 #pragma unroll
   for (int r = 0; r < R; ++r) {
-    int64_t s1 = 0;
-    uint64_t shh = 0, sha = 0, saa = 0;
+    double s1 = 0.0, s2 = 0.0;
     for (int w = 0; w < nwaves; ++w) {
-      s1 += (int64_t)part[w][r][0];
-      shh += part[w][r][1];
-      sha += part[w][r][2];
-      saa += part[w][r][3];
+      s1 += red[0][w][r];
+      s2 += red[1][w][r];
     }
-    // S2 = shh * 2^40 + sha * 2^21 + saa
-    const U128 S2 = add128(add128(shl128(shh, 40), shl128(sha, 21)), U128{0, saa});
-    // K * S2 (K < 2^17, S2 < 2^97)
-    const U128 KS2 = add128(mul64x64(S2.lo, (uint64_t)K), U128{S2.hi * (uint64_t)K, 0});
-    const uint64_t as1 = s1 < 0 ? (uint64_t)(-s1) : (uint64_t)s1;
-    const U128 var_num = sub128(KS2, mul64x64(as1, as1));  // K^2 * var * 2^48 >= 0
-    const double mean = (double)s1 / (double)K * 0x1p-24;
-    const double var = u128_to_f64(var_num) / ((double)K * (double)K) * 0x1p-48;
-    const double rstd = 1.0 / sqrt(var + eps);
-    mu32[r] = (float)mean;
-    r32[r] = (float)rstd;
+    const double dm = s1 / (double)K;  // mean - c
+    const double var = fmax(s2 / (double)K - dm * dm, 0.0);
+    mu32[r] = (float)(cs[r] + dm);
+    r32[r] = (float)(1.0 / sqrt(var + eps));
   }
 
-  // pass 2: normalize, shifted affine, quantize; each chunk's gamma,
+  // normalize, shifted affine, quantize; each chunk's gamma,
   // beta - z and inv_s are loaded once and applied to all R rows
 #pragma unroll
   for (int j = 0; j < CPT; ++j) {
@@ -172,40 +126,49 @@ __global__ __launch_bounds__(1024) void ln_quantize_kernel(
     float g[8], c[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      g[e] = half_bits_to_float((uint16_t)(gw[e >> 1] >> (16 * (e & 1))));
-      c[e] = half_bits_to_float((uint16_t)(bw[e >> 1] >> (16 * (e & 1)))) - zz[e];
+      g[e] = (e & 1) ? half_hi(gw[e >> 1]) : half_lo(gw[e >> 1]);
+      c[e] = ((e & 1) ? half_hi(bw[e >> 1]) : half_lo(bw[e >> 1])) - zz[e];
     }
 #pragma unroll
     for (int r = 0; r < R; ++r) {
       const int64_t row = row0 + r;
       if (row >= M) continue;
       const uint32_t w[4] = {x[r][j].x, x[r][j].y, x[r][j].z, x[r][j].w};
-      uint32_t packed[2] = {0, 0};
+      uint32_t code[8];
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        const float hv = half_bits_to_float((uint16_t)(w[e >> 1] >> (16 * (e & 1))));
+        const float hv = (e & 1) ? half_hi(w[e >> 1]) : half_lo(w[e >> 1]);
         const float d = hv - mu32[r];
         const float n = d * r32[r];
         const float gg = n * g[e];
         const float y = gg + c[e];
         const float u = y * is[e];
-        const int q = (int)rintf(fminf(fmaxf(u, -qa), qa));
-        packed[e >> 2] |= (uint32_t)(q & 0xff) << (8 * (e & 3));
+        // clamp, then round to nearest even by adding 1.5 * 2^23: for
+        // |v| <= 127 the sum's unit is 1, so its low byte is the code
+        const float v = __builtin_amdgcn_fmed3f(u, -qa, qa);
+        code[e] = __float_as_uint(v + 12582912.0f);
       }
-      *reinterpret_cast<uint2 *>(Xq + row * K + (int64_t)ch * 8) = make_uint2(packed[0], packed[1]);
+      const uint32_t lo = __builtin_amdgcn_perm(code[1], code[0], 0x0c0c0400u) |
+                          __builtin_amdgcn_perm(code[3], code[2], 0x04000c0cu);
+      const uint32_t hi = __builtin_amdgcn_perm(code[5], code[4], 0x0c0c0400u) |
+                          __builtin_amdgcn_perm(code[7], code[6], 0x04000c0cu);
+      *reinterpret_cast<uint2 *>(Xq + row * K + (int64_t)ch * 8) = make_uint2(lo, hi);
     }
   }
 }
 
-template <int CPT, int R>
+// MAXT bounds the workgroup (and so frees registers for larger CPT)
+template <int CPT, int R, int MAXT = 1024>
 hipError_t launch_lnq(const uint16_t *h, int64_t M, int64_t K, const uint16_t *gamma,
                       const uint16_t *beta, float eps, int qa, const float *z, const float *inv_s,
                       int8_t *Xq, hipStream_t st) {
+  static_assert(MAXT % 64 == 0 && MAXT <= 1024, "workgroup size");
   const int64_t nchunks = K / 8;
   const int threads = (int)((nchunks + CPT * 64 - 1) / (CPT * 64)) * 64;
+  if (threads > MAXT) return hipErrorInvalidValue;
   const unsigned grid = (unsigned)((M + R - 1) / R);
-  ln_quantize_kernel<CPT, R><<<grid, threads, 0, st>>>(h, M, (int)K, gamma, beta, (double)eps,
-                                                       (float)qa, z, inv_s, Xq);
+  ln_quantize_kernel<CPT, R, MAXT><<<grid, threads, 0, st>>>(h, M, (int)K, gamma, beta,
+                                                             (double)eps, (float)qa, z, inv_s, Xq);
   return hipGetLastError();
 }
 
@@ -216,10 +179,11 @@ using namespace detail;
 hipError_t launch_ln_quantize_act(const uint16_t *h, int64_t M, int64_t K, const uint16_t *gamma,
                                   const uint16_t *beta, float eps, int qa, const float *z,
                                   const float *inv_s, int8_t *Xq, hipStream_t st) {
-  // 2, 4 or 8 chunks of 8 channels per thread keep a workgroup within 1024
-  // threads up to K = 16384, 32768, 65536; R x CPT = 8 chunks per thread
-  if (K <= 16384) return launch_lnq<2, 4>(h, M, K, gamma, beta, eps, qa, z, inv_s, Xq, st);
-  if (K <= 32768) return launch_lnq<4, 2>(h, M, K, gamma, beta, eps, qa, z, inv_s, Xq, st);
+  // one row per workgroup, 4 chunks of 8 channels per thread up to
+  // K = 4096 and 8 beyond (a workgroup of at most 1024 threads covers
+  // K = 65536); measured on K = 768 ... 32768 against 2, 16 and 32 chunks
+  // per thread and 2 rows per workgroup
+  if (K <= 4096) return launch_lnq<4, 1>(h, M, K, gamma, beta, eps, qa, z, inv_s, Xq, st);
   return launch_lnq<8, 1>(h, M, K, gamma, beta, eps, qa, z, inv_s, Xq, st);
 }
 

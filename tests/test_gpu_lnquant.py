@@ -1,6 +1,14 @@
 """GPU parity of ot_ln_quantize_act (LayerNorm fused with symmetrization and
 per-channel quantization, Sec. 3.2) against the CPU oracle, through the C
-ABI: codes are compared bit for bit on every element."""
+ABI.
+
+The oracle takes the row statistics exactly; the kernel sums in float64 in a
+fixed order, so its fp32 mean and rstd can differ from the oracle's by one
+fp32 unit when the exact value lies within a few float64 units of an fp32
+rounding boundary.  Codes are therefore compared bit for bit everywhere
+except inside the window of a rounding tie that such a one-unit change can
+move a value across; there they may differ by one.  (No test case here has
+hit that window so far; the check exists so that the bar is stated.)"""
 import numpy as np
 import pytest
 import torch
@@ -42,6 +50,27 @@ def _random_inputs(M, K, seed, a_bits=8, eps=1e-5):
     return H, gamma, beta, z, inv_s
 
 
+def assert_codes_match(got, H, gamma, beta, eps, z, inv_s, a_bits):
+    qa = O.qmax(a_bits)
+    u = O.ln_scaled_act(H, gamma, beta, eps, z, inv_s).astype(np.float64)
+    ref = np.clip(np.rint(u), -qa, qa)
+    differ = got.astype(np.float64) != ref
+    if not differ.any():
+        return
+    mean, var = O.layernorm_stats(H)
+    mu32 = np.abs(mean.astype(np.float32).astype(np.float64))[:, None]
+    r32 = (1.0 / np.sqrt(var + float(np.float32(eps))))[:, None]
+    g = np.abs(gamma.astype(np.float64))[None, :]
+    i = np.abs(inv_s.astype(np.float64))[None, :]
+    c = np.abs(beta.astype(np.float64) - z.astype(np.float64))[None, :]
+    # a one-unit change of fp32(mean) or fp32(rstd), and the fp32 roundings
+    # after it, move u by at most this much
+    window = 2.0 ** -23 * (2 * mu32 * r32 * g * i + 8 * (np.abs(u) + c * i)) + 2.0 ** -20
+    near_tie = np.abs(np.abs(u - np.trunc(u)) - 0.5) <= window
+    assert np.all(np.abs(got[differ].astype(int) - ref[differ]) <= 1)
+    assert np.all(near_tie[differ]), f"{int((differ & ~near_tie).sum())} codes differ away from a tie"
+
+
 def _run(H, gamma, beta, eps, a_bits, z, inv_s):
     Xq = ot.ln_quantize_act(dev(H), dev(gamma), dev(beta), eps, a_bits, dev(z), dev(inv_s))
     torch.cuda.synchronize()
@@ -59,8 +88,7 @@ def test_parity_random(M, K):
     case(f"ln_quantize M={M} K={K}")
     H, gamma, beta, z, inv_s = _random_inputs(M, K, 100 * M + K)
     got = _run(H, gamma, beta, 1e-5, 8, z, inv_s)
-    ref = O.ln_quantize_act(H, gamma, beta, 1e-5, z, inv_s, 8)
-    assert np.array_equal(got, ref)
+    assert_codes_match(got, H, gamma, beta, 1e-5, z, inv_s, 8)
 
 
 @pytest.mark.parametrize("a_bits", [6, 4, 2])
@@ -68,8 +96,7 @@ def test_parity_low_bits(a_bits):
     case(f"ln_quantize a_bits={a_bits}")
     H, gamma, beta, z, inv_s = _random_inputs(40, 2064, 7 + a_bits, a_bits)
     got = _run(H, gamma, beta, 1e-5, a_bits, z, inv_s)
-    ref = O.ln_quantize_act(H, gamma, beta, 1e-5, z, inv_s, a_bits)
-    assert np.array_equal(got, ref)
+    assert_codes_match(got, H, gamma, beta, 1e-5, z, inv_s, a_bits)
     assert np.abs(got).max() <= O.qmax(a_bits)
 
 
@@ -96,15 +123,13 @@ def test_parity_extreme_rows():
     inv_s = r.uniform(10, 40, K).astype(np.float32)
     for eps in (1e-5, 1e-12, 1.0):
         got = _run(H, gamma, beta, eps, 8, z, inv_s)
-        ref = O.ln_quantize_act(H, gamma, beta, eps, z, inv_s, 8)
-        assert np.array_equal(got, ref), f"eps={eps}"
+        assert_codes_match(got, H, gamma, beta, eps, z, inv_s, 8)
 
 
 def test_eps_zero_on_rows_with_spread():
     case("ln_quantize eps=0")
     H, gamma, beta, z, inv_s = _random_inputs(16, 768, 21)
-    assert np.array_equal(_run(H, gamma, beta, 0.0, 8, z, inv_s),
-                          O.ln_quantize_act(H, gamma, beta, 0.0, z, inv_s, 8))
+    assert_codes_match(_run(H, gamma, beta, 0.0, 8, z, inv_s), H, gamma, beta, 0.0, z, inv_s, 8)
 
 
 @pytest.mark.parametrize("name,li", [("opt125m_w8a8", 0), ("opt6.7b_w8a8", 2),
@@ -121,7 +146,7 @@ def test_parity_workload_inputs(name, li):
     _, z, s, inv_s = O.calibrate(calib, wl.a_bits)
     H = synth.ln_inputs(wl, li, 24)
     got = _run(H, gamma, beta, 1e-5, wl.a_bits, z, inv_s)
-    assert np.array_equal(got, O.ln_quantize_act(H, gamma, beta, 1e-5, z, inv_s, wl.a_bits))
+    assert_codes_match(got, H, gamma, beta, 1e-5, z, inv_s, wl.a_bits)
 
 
 def test_fullsize_opt13b_qkv_input_sampled_rows():
@@ -143,7 +168,7 @@ def test_fullsize_opt13b_qkv_input_sampled_rows():
     rows = np.array(sorted(set(np.random.default_rng(1).choice(M, 48, replace=False).tolist())
                            | {0, M - 1}))
     got = Xq.index_select(0, torch.from_numpy(rows).cuda()).cpu().numpy()
-    assert np.array_equal(got, O.ln_quantize_act(H[rows], gamma, beta, 1e-5, z, inv_s, wl.a_bits))
+    assert_codes_match(got, H[rows], gamma, beta, 1e-5, z, inv_s, wl.a_bits)
 
 
 def test_close_to_unfused_layernorm_then_quantize():
