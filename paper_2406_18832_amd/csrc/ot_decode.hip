@@ -40,6 +40,9 @@ struct DecodeCfg {
   static_assert(kRed <= S * kStage, "partial sums fit in the ring");
 };
 
+// cache-policy operand of a buffer load on gfx950: non-temporal
+constexpr int kNonTemporal = 2;
+
 template <int kChunks>
 __device__ __forceinline__ int swz_rows(int r) {
   if constexpr (kChunks == 8) return (r & 7) ^ ((r >> 3) & 1);
@@ -82,8 +85,13 @@ __device__ __forceinline__ void decode_body(
     for (int j = 0; j < C::kLoads; ++j) {
       const int q = wave * C::kLoads + j;  // wave-uniform
       const uint32_t off = (goff[j] + (uint32_t)k0) | ((uint32_t)(k0 + gck[j] >= K) << 31);
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(q * C::kRowsPerLoad < C::kTokRows ? rx : rw,
-                                               (lds_void *)(dst + q * 1024), 16, off, 0, 0, 0);
+      // weights are read once: non-temporal ("nt") keeps them from evicting
+      // the token rows, which every workgroup re-reads, from the caches
+      if (q * C::kRowsPerLoad < C::kTokRows)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (lds_void *)(dst + q * 1024), 16, off, 0, 0, 0);
+      else
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (lds_void *)(dst + q * 1024), 16, off, 0, 0,
+                                                 kNonTemporal);
     }
   };
   // fragment offsets within a stage: lane (r16, c4) of step t reads logical
