@@ -35,6 +35,13 @@ ln_scaled_act   LayerNorm with the shift z taken into its bias (Sec. 3.2:
                 z combined with the LayerNorm bias), divided by s per
                 channel, without an fp16 round trip.
 ln_quantize_act Eq. (g)'s per-channel codes of that value.
+quantize_act_per_token  Eq. (c): dynamic per-token scales s^X_m for the
+                linears without activation outliers (out, fc2; Sec. 3.2
+                and Sec. 4.1), and the codes round(X / s^X).
+fold_weights_per_token  Eq. (c) and Eq. (h): per-output-channel weight
+                scales without an activation scale, and the bias b + z that
+                carries a symmetrized residual stream back (Eq. (h)).
+epilogue_per_token      Eq. (c): s^X_m s^W_n times the integer sum, plus b'.
 reference_fp64, folded_fp64     exact-arithmetic references (tests only).
 
 Readings taken where the paper is silent (each applies to both this oracle
@@ -355,6 +362,72 @@ def ln_quantize_act(H, gamma, beta, eps, z, inv_s, a_bits: int):
     qa = qmax(a_bits)
     u = ln_scaled_act(H, gamma, beta, eps, z, inv_s)
     return np.clip(np.rint(u), -qa, qa).astype(np.int8)
+
+
+# --------------------------------------------------------------------------
+# Per-token path for the linears without activation outliers (Eq. (c), (h))
+# --------------------------------------------------------------------------
+def quantize_act_per_token(X, a_bits: int):
+    """Dynamic per-token symmetric quantization, Eq. (c) (Sec. 4.1: per-token
+    symmetric for the activations that are not LayerNorm outputs).
+
+    Per row m: s_m = fp32(max_k |x_mk| / qa) (float64 division; s_m = 1 for
+    a row of zeros), inv_m = fp32(1 / s_m) (float64), and
+      q = clip(round(fp32(x) * inv_m), -qa, qa)   (float32 multiply, RNE).
+    Returns (Xq int8 [M, K], s float32 [M]).
+    """
+    qa = qmax(a_bits)
+    X = np.asarray(X)
+    if X.dtype != np.float16 or X.ndim != 2:
+        raise ValueError("X must be fp16 [M, K]")
+    mx = np.abs(X.astype(np.float64)).max(axis=1)
+    s = (mx / float(qa)).astype(np.float32)
+    s[s == 0] = np.float32(1.0)
+    inv = (1.0 / s.astype(np.float64)).astype(np.float32)
+    u = X.astype(np.float32) * inv[:, None]
+    assert u.dtype == np.float32
+    return np.clip(np.rint(u), -qa, qa).astype(np.int8), s
+
+
+def fold_weights_per_token(W, b, zres, w_bits: int):
+    """Weights of a per-token linear (Eq. (c)): no activation scale to fold.
+
+      sW_n = max_k |W[n, k]| / qw        (float64, stored float32; 1 for a
+                                          zero row)
+      Wq   = clip(round(W / sW_n), -qw, qw)     correctly rounded fp64 division
+      b'_n = b_n + zres_n                 Eq. (h): with a symmetrized residual
+                                          stream X_res - z, its shift z comes
+                                          back through the bias
+    ``b`` and ``zres`` may be None (zero).  b' is summed in float64 and
+    stored float32.  Returns (Wq int8 [N, K], sW float32 [N], b' float32 [N]).
+    """
+    qw = qmax(w_bits)
+    W = np.asarray(W)
+    if W.dtype != np.float16 or W.ndim != 2:
+        raise ValueError("W must be fp16 [N, K]")
+    N, K = W.shape
+    W64 = W.astype(np.float64)
+    b64 = np.zeros(N) if b is None else np.asarray(b).astype(np.float64)
+    if not (np.all(np.isfinite(W64)) and np.all(np.isfinite(b64))):
+        raise NonFinite("non-finite weights or bias")
+    z64 = np.zeros(N) if zres is None else np.asarray(zres, dtype=np.float32).astype(np.float64)
+    assert z64.shape == (N,)
+    sW = (np.abs(W64).max(axis=1) / float(qw)).astype(np.float32)
+    sW[sW == 0] = np.float32(1.0)
+    Wq = np.clip(np.rint(W64 / sW.astype(np.float64)[:, None]), -qw, qw).astype(np.int8)
+    bprime = (b64 + z64).astype(np.float32)
+    return Wq, sW, bprime
+
+
+def epilogue_per_token(acc, sX, sW, bprime):
+    """Eq. (c) with the bias: y = fp16(fp32(fp32(fp32(acc) * sX_m) * sW_n)
+    + b'_n), each float32 operation rounded to nearest even."""
+    a = np.asarray(acc, dtype=np.int64).astype(np.float32)
+    t = a * np.asarray(sX, dtype=np.float32)[:, None]
+    p = t * np.asarray(sW, dtype=np.float32)[None, :]
+    y = p + np.asarray(bprime, dtype=np.float32)[None, :]
+    assert y.dtype == np.float32
+    return y.astype(np.float16)
 
 
 def pipeline(X, W, b, calib_batches, a_bits: int, w_bits: int):
