@@ -183,6 +183,53 @@ ot_status ot_qlinear(const int8_t *Xq, const int8_t *Wq, const float *sW,
                      int a_bits, int w_bits, uint16_t *Y, int32_t *acc_out,
                      void *workspace, void *stream);
 
+/*
+ * Per-token path.  The paper keeps the linears without activation outliers
+ * (out and fc2, whose inputs are not LayerNorm outputs) on per-token
+ * symmetric activation quantization, Eq. (c), and carries a symmetrized
+ * residual stream back through their bias, Eq. (h) (Sec. 3.2, Sec. 4.1).
+ *
+ * ot_quantize_act_per_token -- dynamic per-token scales and codes:
+ *   sX[m]    = fp32(max_k |x[m,k]| / qa)   (fp64 division; 1 for a zero row)
+ *   Xq[m,k]  = clip(rne(fp32(x[m,k]) * fp32(1 / sX[m])), -qa, qa)
+ *   x   [M x K] fp16 (device), finite.  M >= 0 (0 is a no-op),
+ *       16 <= K <= 65536, K % 16 == 0.
+ *   Xq  [M x K] int8 output, sX [M] fp32 output (device).
+ * Asynchronous on stream.
+ */
+ot_status ot_quantize_act_per_token(const uint16_t *x, int64_t M, int64_t K,
+                                    int a_bits, int8_t *Xq, float *sX,
+                                    void *stream);
+
+/*
+ * ot_fold_weights_per_token -- offline weights of a per-token linear: no
+ * activation scale is folded in (Eq. (c)).
+ *   sW[n]     = fp32(max_k |W[n,k]| / qw)   (1 for a zero row)
+ *   Wq[n,k]   = clip(rne(W[n,k] / sW[n]), -qw, qw)  (correctly rounded fp64)
+ *   bprime[n] = fp32(b[n] + zres[n])        (fp64 sum; Eq. (h))
+ *   W [N x K] fp16, b [N] fp16 or NULL, zres [N] fp32 or NULL: the shift z
+ *   of the symmetrized residual stream that this linear's output is added
+ *   to (NULL when the residual stream is not symmetrized).
+ * Synchronous.  OT_ENONFINITE if W, b or zres hold a NaN or an infinity.
+ */
+ot_status ot_fold_weights_per_token(const uint16_t *W, const uint16_t *b,
+                                    const float *zres, int64_t N, int64_t K,
+                                    int w_bits, int8_t *Wq, float *sW,
+                                    float *bprime, void *stream);
+
+/*
+ * ot_qlinear_per_token -- the quantized linear of Eq. (c) with the bias:
+ *   Y[m,n] = fp16(fp32(fp32(fp32(acc[m,n]) * sX[m]) * sW[n]) + bprime[n])
+ * with acc = Xq Wq^T exact in int32, each fp32 operation rounded to nearest
+ * even.  Arguments as for ot_qlinear, plus sX [M] fp32 (device) from
+ * ot_quantize_act_per_token; same kernels, same error codes.
+ */
+ot_status ot_qlinear_per_token(const int8_t *Xq, const int8_t *Wq,
+                               const float *sX, const float *sW,
+                               const float *bprime, int64_t M, int64_t N,
+                               int64_t K, int a_bits, int w_bits, uint16_t *Y,
+                               int32_t *acc_out, void *workspace, void *stream);
+
 /* Bytes of optional scratch ot_qlinear can use for these sizes (0 if none). */
 size_t ot_qlinear_workspace_size(int64_t M, int64_t N, int64_t K);
 

@@ -67,6 +67,22 @@ ot_status ot_calibrate(const uint16_t *x, int64_t rows, int64_t K, int a_bits, i
   return hip_status(hipStreamSynchronize(st));
 }
 
+// Reads sW and b' back (synchronously): a NaN scale marks non-finite weights,
+// a non-finite b' non-finite bias or shift.
+static ot_status fold_outputs_finite(const float *sW, const float *bprime, int64_t N,
+                                     hipStream_t st) {
+  ot_status rc;
+  std::vector<float> scale((size_t)N), bias((size_t)N);
+  if ((rc = hip_status(hipMemcpyAsync(scale.data(), sW, sizeof(float) * N, hipMemcpyDeviceToHost,
+                                      st))) != OT_OK ||
+      (rc = hip_status(hipMemcpyAsync(bias.data(), bprime, sizeof(float) * N,
+                                      hipMemcpyDeviceToHost, st))) != OT_OK)
+    return rc;
+  if ((rc = hip_status(hipStreamSynchronize(st))) != OT_OK) return rc;
+  if (!all_finite(scale) || !all_finite(bias)) return OT_ENONFINITE;
+  return OT_OK;
+}
+
 ot_status ot_fold_weights(const uint16_t *W, const uint16_t *b, int64_t N, int64_t K, int w_bits,
                           const float *z, const float *s, int8_t *Wq, float *sW, float *bprime,
                           void *stream) {
@@ -78,15 +94,7 @@ ot_status ot_fold_weights(const uint16_t *W, const uint16_t *b, int64_t N, int64
   if ((rc = hip_status(ot::launch_fold(W, b, N, K, qmax(w_bits), z, s, Wq, sW, bprime, st))) !=
       OT_OK)
     return rc;
-  std::vector<float> scale((size_t)N), bias((size_t)N);
-  if ((rc = hip_status(hipMemcpyAsync(scale.data(), sW, sizeof(float) * N, hipMemcpyDeviceToHost,
-                                      st))) != OT_OK ||
-      (rc = hip_status(hipMemcpyAsync(bias.data(), bprime, sizeof(float) * N,
-                                      hipMemcpyDeviceToHost, st))) != OT_OK)
-    return rc;
-  if ((rc = hip_status(hipStreamSynchronize(st))) != OT_OK) return rc;
-  if (!all_finite(scale) || !all_finite(bias)) return OT_ENONFINITE;
-  return OT_OK;
+  return fold_outputs_finite(sW, bprime, N, st);
 }
 
 ot_status ot_quantize_act(const uint16_t *x, int64_t M, int64_t K, int a_bits, const float *z,
@@ -128,7 +136,51 @@ ot_status ot_qlinear(const int8_t *Xq, const int8_t *Wq, const float *sW, const 
   if (!aligned16(Xq) || !aligned16(Wq) || !aligned16(sW) || !aligned16(bprime) || !aligned16(Y) ||
       (acc_out && !aligned16(acc_out)))
     return OT_EINVAL;
-  return hip_status(ot::launch_qgemm(Xq, Wq, sW, bprime, M, N, K, Y, acc_out,
+  return hip_status(ot::launch_qgemm(Xq, Wq, nullptr, sW, bprime, M, N, K, Y, acc_out,
+                                     static_cast<hipStream_t>(stream)));
+}
+
+ot_status ot_quantize_act_per_token(const uint16_t *x, int64_t M, int64_t K, int a_bits,
+                                    int8_t *Xq, float *sX, void *stream) {
+  if (!bits_ok(a_bits) || M < 0 || K < 0) return OT_EINVAL;
+  if (K < 16 || K % 16 != 0 || K > kMaxLnK || M > kMaxRows) return OT_ESHAPE;
+  if (M == 0) return OT_OK;
+  if (!x || !Xq || !sX) return OT_EINVAL;
+  if (!aligned16(x) || !aligned16(Xq) || !aligned16(sX)) return OT_EINVAL;
+  return hip_status(ot::launch_quantize_act_per_token(x, M, K, qmax(a_bits), Xq, sX,
+                                                      static_cast<hipStream_t>(stream)));
+}
+
+ot_status ot_fold_weights_per_token(const uint16_t *W, const uint16_t *b, const float *zres,
+                                    int64_t N, int64_t K, int w_bits, int8_t *Wq, float *sW,
+                                    float *bprime, void *stream) {
+  if (!bits_ok(w_bits) || N < 0 || K < 0) return OT_EINVAL;
+  if (N == 0 || K == 0 || N > kMaxRows || K > kMaxRows) return OT_ESHAPE;
+  if (!W || !Wq || !sW || !bprime) return OT_EINVAL;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  ot_status rc;
+  if ((rc = hip_status(ot::launch_fold_per_token(W, b, zres, N, K, qmax(w_bits), Wq, sW, bprime,
+                                                 st))) != OT_OK)
+    return rc;
+  return fold_outputs_finite(sW, bprime, N, st);
+}
+
+ot_status ot_qlinear_per_token(const int8_t *Xq, const int8_t *Wq, const float *sX,
+                               const float *sW, const float *bprime, int64_t M, int64_t N,
+                               int64_t K, int a_bits, int w_bits, uint16_t *Y, int32_t *acc_out,
+                               void *workspace, void *stream) {
+  (void)workspace;
+  if (!bits_ok(a_bits) || !bits_ok(w_bits) || M < 0 || N < 0 || K < 0) return OT_EINVAL;
+  if (N == 0 || K < 16 || K % 16 != 0 || K > kMaxK || M > kMaxRows || N > kMaxRows)
+    return OT_ESHAPE;
+  if ((M + 255) / 256 * ((N + 255) / 256) > kMaxRows) return OT_ESHAPE;
+  if (K * qmax(a_bits) * qmax(w_bits) >= (int64_t(1) << 31)) return OT_ERANGE;
+  if (M == 0) return OT_OK;
+  if (!Xq || !Wq || !sX || !sW || !bprime || !Y) return OT_EINVAL;
+  if (!aligned16(Xq) || !aligned16(Wq) || !aligned16(sW) || !aligned16(bprime) || !aligned16(Y) ||
+      (acc_out && !aligned16(acc_out)))
+    return OT_EINVAL;
+  return hip_status(ot::launch_qgemm(Xq, Wq, sX, sW, bprime, M, N, K, Y, acc_out,
                                      static_cast<hipStream_t>(stream)));
 }
 

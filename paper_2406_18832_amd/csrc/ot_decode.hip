@@ -49,11 +49,11 @@ __device__ __forceinline__ int swz_rows(int r) {
   else return r & 15;
 }
 
-template <int MB, int NR, int NK, int RBW, int BKD, int S>
+template <int MB, int NR, int NK, int RBW, int BKD, int S, bool PT>
 __device__ __forceinline__ void decode_body(
     int8_t *smem, const int8_t *__restrict__ Xq, const int8_t *__restrict__ Wq,
-    const float *__restrict__ sW, const float *__restrict__ bp, int M, int N, int K,
-    uint16_t *__restrict__ Y, int32_t *__restrict__ acc_out) {
+    const float *__restrict__ sX, const float *__restrict__ sW, const float *__restrict__ bp,
+    int M, int N, int K, uint16_t *__restrict__ Y, int32_t *__restrict__ acc_out) {
   using C = DecodeCfg<MB, NR, NK, RBW, BKD, S>;
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -173,33 +173,41 @@ __device__ __forceinline__ void decode_body(
 
   // 16x16 output blocks: lane l holds token l%16 and channels 4*(l/16) + r
 #pragma unroll
-  for (int i = 0; i < RBW; ++i)
+  for (int j = 0; j < MB; ++j) {
+    const int m = j * 16 + r16;
+    const float sx = (PT && m < M) ? sX[m] : 0.f;
 #pragma unroll
-    for (int j = 0; j < MB; ++j) {
-      const int64_t m = j * 16 + r16;
+    for (int i = 0; i < RBW; ++i) {
       const int64_t n = nwg0 + (rg * RBW + i) * 16 + 4 * c4;
-      store4(Y, acc_out, sW, bp, m, n, M, N, acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
+      store4<PT>(Y, acc_out, sW, bp, sx, m, n, M, N, acc[i][j][0], acc[i][j][1], acc[i][j][2],
+                 acc[i][j][3]);
     }
+  }
 }
 
-template <int MB, int NR, int NK, int RBW, int BKD, int S>
+template <int MB, int NR, int NK, int RBW, int BKD, int S, bool PT>
 __global__ __launch_bounds__(64 * NR * NK) void qgemm_decode_kernel(
-    const int8_t *__restrict__ Xq, const int8_t *__restrict__ Wq, const float *__restrict__ sW,
-    const float *__restrict__ bp, int M, int N, int K, uint16_t *__restrict__ Y,
-    int32_t *__restrict__ acc_out) {
+    const int8_t *__restrict__ Xq, const int8_t *__restrict__ Wq, const float *__restrict__ sX,
+    const float *__restrict__ sW, const float *__restrict__ bp, int M, int N, int K,
+    uint16_t *__restrict__ Y, int32_t *__restrict__ acc_out) {
   __shared__ __attribute__((aligned(1024)))
   int8_t smem[S * DecodeCfg<MB, NR, NK, RBW, BKD, S>::kStage];
-  decode_body<MB, NR, NK, RBW, BKD, S>(smem, Xq, Wq, sW, bp, M, N, K, Y, acc_out);
+  decode_body<MB, NR, NK, RBW, BKD, S, PT>(smem, Xq, Wq, sX, sW, bp, M, N, K, Y, acc_out);
 }
 
+// sX == nullptr: per-channel epilogue; else per-token scales sX [M].
 template <int MB, int NR, int NK, int RBW, int BKD, int S>
-hipError_t launch_decode(const int8_t *Xq, const int8_t *Wq, const float *sW, const float *bp,
-                          int64_t M, int64_t N, int64_t K, uint16_t *Y, int32_t *acc_out,
-                          hipStream_t st) {
+hipError_t launch_decode(const int8_t *Xq, const int8_t *Wq, const float *sX, const float *sW,
+                         const float *bp, int64_t M, int64_t N, int64_t K, uint16_t *Y,
+                         int32_t *acc_out, hipStream_t st) {
   constexpr int rows = 16 * RBW * NR;
   const unsigned grid = (unsigned)((N + rows - 1) / rows);
-  qgemm_decode_kernel<MB, NR, NK, RBW, BKD, S><<<grid, 64 * NR * NK, 0, st>>>(
-      Xq, Wq, sW, bp, (int)M, (int)N, (int)K, Y, acc_out);
+  if (sX)
+    qgemm_decode_kernel<MB, NR, NK, RBW, BKD, S, true><<<grid, 64 * NR * NK, 0, st>>>(
+        Xq, Wq, sX, sW, bp, (int)M, (int)N, (int)K, Y, acc_out);
+  else
+    qgemm_decode_kernel<MB, NR, NK, RBW, BKD, S, false><<<grid, 64 * NR * NK, 0, st>>>(
+        Xq, Wq, sX, sW, bp, (int)M, (int)N, (int)K, Y, acc_out);
   return hipGetLastError();
 }
 
@@ -207,9 +215,9 @@ hipError_t launch_decode(const int8_t *Xq, const int8_t *Wq, const float *sW, co
 
 using namespace detail;
 
-hipError_t launch_qgemm_decode(const int8_t *Xq, const int8_t *Wq, const float *sW,
-                               const float *bprime, int64_t M, int64_t N, int64_t K,
-                               uint16_t *Y, int32_t *acc_out, hipStream_t st) {
+hipError_t launch_qgemm_decode(const int8_t *Xq, const int8_t *Wq, const float *sX,
+                               const float *sW, const float *bprime, int64_t M, int64_t N,
+                               int64_t K, uint16_t *Y, int32_t *acc_out, hipStream_t st) {
   // Template arguments
   // <token blocks, row groups, K groups, row blocks per wave, BKD, stages>.
   // Up to 16 tokens the workgroup is one 16-row block split over 4 K groups
@@ -219,17 +227,17 @@ hipError_t launch_qgemm_decode(const int8_t *Xq, const int8_t *Wq, const float *
   // pass over the 256 CUs (taller tiles re-read the token tile less, shorter
   // ones use more CUs); past 128 rows x 256 CUs, 64-row tiles keep the last
   // pass's tail short.
-  if (M <= 16) return launch_decode<1, 1, 4, 1, 256, 4>(Xq, Wq, sW, bprime, M, N, K, Y, acc_out, st);
+  if (M <= 16) return launch_decode<1, 1, 4, 1, 256, 4>(Xq, Wq, sX, sW, bprime, M, N, K, Y, acc_out, st);
   constexpr int64_t kCUs = 256;
   const int rows = N <= 32 * kCUs ? 32 : N <= 64 * kCUs ? 64 : N <= 128 * kCUs ? 128 : 64;
   if (M <= 32) {
-    if (rows == 32) return launch_decode<2, 2, 4, 1, 256, 4>(Xq, Wq, sW, bprime, M, N, K, Y, acc_out, st);
-    if (rows == 64) return launch_decode<2, 4, 2, 1, 256, 3>(Xq, Wq, sW, bprime, M, N, K, Y, acc_out, st);
-    return launch_decode<2, 4, 2, 2, 256, 3>(Xq, Wq, sW, bprime, M, N, K, Y, acc_out, st);
+    if (rows == 32) return launch_decode<2, 2, 4, 1, 256, 4>(Xq, Wq, sX, sW, bprime, M, N, K, Y, acc_out, st);
+    if (rows == 64) return launch_decode<2, 4, 2, 1, 256, 3>(Xq, Wq, sX, sW, bprime, M, N, K, Y, acc_out, st);
+    return launch_decode<2, 4, 2, 2, 256, 3>(Xq, Wq, sX, sW, bprime, M, N, K, Y, acc_out, st);
   }
-  if (rows == 32) return launch_decode<4, 2, 4, 1, 256, 4>(Xq, Wq, sW, bprime, M, N, K, Y, acc_out, st);
-  if (rows == 64) return launch_decode<4, 4, 2, 1, 256, 3>(Xq, Wq, sW, bprime, M, N, K, Y, acc_out, st);
-  return launch_decode<4, 4, 2, 2, 256, 3>(Xq, Wq, sW, bprime, M, N, K, Y, acc_out, st);
+  if (rows == 32) return launch_decode<4, 2, 4, 1, 256, 4>(Xq, Wq, sX, sW, bprime, M, N, K, Y, acc_out, st);
+  if (rows == 64) return launch_decode<4, 4, 2, 1, 256, 3>(Xq, Wq, sX, sW, bprime, M, N, K, Y, acc_out, st);
+  return launch_decode<4, 4, 2, 2, 256, 3>(Xq, Wq, sX, sW, bprime, M, N, K, Y, acc_out, st);
 }
 
 }  // namespace ot

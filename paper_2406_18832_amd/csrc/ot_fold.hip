@@ -5,6 +5,8 @@
 //                      min-max scale sW_n = max_k |W_s[n, k]| / qw
 //   Sec. 3.2 Eq. (g):  compensated bias b'_n = sum_k z_k W[n, k] + b_n
 //   Implementation paragraph: done once, before inference.
+// and, for the per-token linears (out, fc2; Eq. (c), (h)), the same
+// per-output-channel quantization of W itself with the bias b + z.
 //
 // One workgroup per output channel n.  Pass 1 reduces max |W_s| and the
 // bias sum in fp64 (each product is exact in fp64: 24 x 11 significand
@@ -21,8 +23,12 @@ namespace detail {
 
 constexpr int kThreads = 256;
 
+// s == nullptr means s = 1 (no activation scale to fold: the per-token
+// path), z == nullptr means z = 0; zres (nullable, [N]) is added to the bias
+// (Eq. (h): the shift of a symmetrized residual stream).
 __global__ __launch_bounds__(kThreads) void fold_kernel(const uint16_t *__restrict__ W,
                                                         const uint16_t *__restrict__ b,
+                                                        const float *__restrict__ zres,
                                                         int64_t K, int qw,
                                                         const float *__restrict__ z,
                                                         const float *__restrict__ s,
@@ -43,9 +49,9 @@ __global__ __launch_bounds__(kThreads) void fold_kernel(const uint16_t *__restri
   for (int64_t k = t; k < K; k += kThreads) {
     const double wk = (double)half_bits_to_float(w[k]);
     bad |= !isfinite(wk);
-    const double ws = (double)s[k] * wk;  // Eq. (e), exact
+    const double ws = s ? (double)s[k] * wk : wk;  // Eq. (e), exact
     m = fmax(m, fabs(ws));
-    acc += (double)z[k] * wk;  // exact product, fp64 sum
+    if (z) acc += (double)z[k] * wk;  // exact product, fp64 sum
   }
   red_max[t] = m;
   red_sum[t] = acc;
@@ -64,7 +70,7 @@ __global__ __launch_bounds__(kThreads) void fold_kernel(const uint16_t *__restri
     if (sw == 0.0f) sw = 1.0f;
     const double bn = b ? (double)half_bits_to_float(b[n]) : 0.0;
     sW[n] = red_bad[0] ? __builtin_nanf("") : sw;  // the host checks sW
-    bprime[n] = (float)(red_sum[0] + bn);
+    bprime[n] = (float)(red_sum[0] + bn + (zres ? (double)zres[n] : 0.0));
     row_scale = (double)sw;
   }
   __syncthreads();
@@ -72,7 +78,8 @@ __global__ __launch_bounds__(kThreads) void fold_kernel(const uint16_t *__restri
   const double lim = (double)qw;
   int8_t *q = Wq + n * K;
   for (int64_t k = t; k < K; k += kThreads) {
-    const double ws = (double)s[k] * (double)half_bits_to_float(w[k]);
+    const double wk = (double)half_bits_to_float(w[k]);
+    const double ws = s ? (double)s[k] * wk : wk;
     const double r = fmin(fmax(rint(ws / sc), -lim), lim);
     q[k] = (int8_t)(int)r;
   }
@@ -85,7 +92,17 @@ using namespace detail;
 hipError_t launch_fold(const uint16_t *W, const uint16_t *b, int64_t N, int64_t K, int qw,
                        const float *z, const float *s, int8_t *Wq, float *sW, float *bprime,
                        hipStream_t st) {
-  fold_kernel<<<(unsigned)N, kThreads, 0, st>>>(W, b, K, qw, z, s, Wq, sW, bprime);
+  fold_kernel<<<(unsigned)N, kThreads, 0, st>>>(W, b, nullptr, K, qw, z, s, Wq, sW, bprime);
+  return hipGetLastError();
+}
+
+// Per-token linear (Eq. (c), (h)): sW_n = max_k |W[n, k]| / qw, codes of W
+// itself, b'_n = b_n + zres_n.
+hipError_t launch_fold_per_token(const uint16_t *W, const uint16_t *b, const float *zres,
+                                 int64_t N, int64_t K, int qw, int8_t *Wq, float *sW,
+                                 float *bprime, hipStream_t st) {
+  fold_kernel<<<(unsigned)N, kThreads, 0, st>>>(W, b, zres, K, qw, nullptr, nullptr, Wq, sW,
+                                                bprime);
   return hipGetLastError();
 }
 

@@ -38,26 +38,47 @@ __device__ inline uint16_t dequant(int a, float sw, float bp) {
   return float_to_half_bits(y);
 }
 
-// Writes four consecutive channels n..n+3 of token m.
+// Per-token path, Eq. (c): y = fp16(fp32(fp32(fp32(acc) * sX_m) * sW_n) + b'_n).
+__device__ inline uint16_t dequant_pt(int a, float sx, float sw, float bp) {
+  const float v = (float)a;
+  const float t = v * sx;
+  const float p = t * sw;
+  const float y = p + bp;
+  return float_to_half_bits(y);
+}
+
+// Epilogue flavours: PT = false is the per-channel path (one scale per
+// output channel), PT = true the per-token path (token scale sx as well).
+template <bool PT>
+__device__ inline uint16_t dequant_x(int a, float sx, float sw, float bp) {
+  if constexpr (PT) return dequant_pt(a, sx, sw, bp);
+  else return dequant(a, sw, bp);
+}
+
+// Writes four consecutive channels n..n+3 of token m (token scale sx, used
+// when PT).
+template <bool PT>
 __device__ inline void store4(uint16_t *__restrict__ Y, int32_t *__restrict__ acc_out,
                               const float *__restrict__ sW, const float *__restrict__ bp,
-                              int64_t m, int64_t n, int64_t M, int64_t N, int a0, int a1, int a2,
-                              int a3) {
+                              float sx, int64_t m, int64_t n, int64_t M, int64_t N, int a0,
+                              int a1, int a2, int a3) {
   if (m >= M) return;
   const int64_t base = m * N + n;
   if (n + 3 < N && (N & 3) == 0) {
     const float4 s4 = *reinterpret_cast<const float4 *>(sW + n);
     const float4 b4 = *reinterpret_cast<const float4 *>(bp + n);
     uint2 o;
-    o.x = (uint32_t)dequant(a0, s4.x, b4.x) | ((uint32_t)dequant(a1, s4.y, b4.y) << 16);
-    o.y = (uint32_t)dequant(a2, s4.z, b4.z) | ((uint32_t)dequant(a3, s4.w, b4.w) << 16);
+    o.x = (uint32_t)dequant_x<PT>(a0, sx, s4.x, b4.x) |
+          ((uint32_t)dequant_x<PT>(a1, sx, s4.y, b4.y) << 16);
+    o.y = (uint32_t)dequant_x<PT>(a2, sx, s4.z, b4.z) |
+          ((uint32_t)dequant_x<PT>(a3, sx, s4.w, b4.w) << 16);
     *reinterpret_cast<uint2 *>(Y + base) = o;
     if (acc_out) *reinterpret_cast<int4 *>(acc_out + base) = make_int4(a0, a1, a2, a3);
   } else {
     const int a[4] = {a0, a1, a2, a3};
     for (int i = 0; i < 4; ++i) {
       if (n + i < N) {
-        Y[base + i] = dequant(a[i], sW[n + i], bp[n + i]);
+        Y[base + i] = dequant_x<PT>(a[i], sx, sW[n + i], bp[n + i]);
         if (acc_out) acc_out[base + i] = a[i];
       }
     }

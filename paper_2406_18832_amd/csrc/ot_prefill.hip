@@ -79,12 +79,12 @@ __device__ __forceinline__ void sched_interleave() {
 
 // The kernel body lives in a device function: hipcc drops the host stub of a
 // kernel template whose body holds lambdas.
-template <int BN, int BM, int BK, int WN, int WM, int S>
+template <int BN, int BM, int BK, int WN, int WM, int S, bool PT>
 __device__ __forceinline__ void prefill_body(
     int8_t *smem, const int8_t *__restrict__ Xq, const int8_t *__restrict__ Wq,
-    const float *__restrict__ sW, const float *__restrict__ bp, int M, int N, int K,
-    uint16_t *__restrict__ Y, int32_t *__restrict__ acc_out, int tiles_m, int tiles_n,
-    int group_m) {
+    const float *__restrict__ sX, const float *__restrict__ sW, const float *__restrict__ bp,
+    int M, int N, int K, uint16_t *__restrict__ Y, int32_t *__restrict__ acc_out, int tiles_m,
+    int tiles_n, int group_m) {
   using C = PrefillCfg<BN, BM, BK, WN, WM, S>;
 
   // ---- tile schedule ------------------------------------------------------
@@ -225,6 +225,13 @@ __device__ __forceinline__ void prefill_body(
   // and rows 8*(r/4) + 4*(l/32) + (r mod 4) for register r.  Columns are
   // tokens here and rows are channels, so registers 4j..4j+3 are four
   // consecutive channels of one token.
+  // token scales of this lane's tokens (per-token path only)
+  float sx[C::kFM];
+#pragma unroll
+  for (int g = 0; g < C::kFM; ++g) {
+    const int m = m0 + wm * C::kTM + g * 32 + fr;
+    sx[g] = (PT && m < M) ? sX[m] : 0.f;
+  }
   if (acc_out != nullptr) {  // test path: also stores the raw accumulators
 #pragma unroll
     for (int f = 0; f < C::kFN; ++f)
@@ -234,8 +241,8 @@ __device__ __forceinline__ void prefill_body(
 #pragma unroll
         for (int g = 0; g < C::kFM; ++g) {
           const int64_t m = m0 + wm * C::kTM + g * 32 + fr;
-          store4(Y, acc_out, sW, bp, m, n, M, N, acc[f][g][4 * j], acc[f][g][4 * j + 1],
-                 acc[f][g][4 * j + 2], acc[f][g][4 * j + 3]);
+          store4<PT>(Y, acc_out, sW, bp, sx[g], m, n, M, N, acc[f][g][4 * j],
+                     acc[f][g][4 * j + 1], acc[f][g][4 * j + 2], acc[f][g][4 * j + 3]);
         }
       }
     return;
@@ -275,10 +282,10 @@ __device__ __forceinline__ void prefill_body(
       for (int g = 0; g < C::kFM; ++g) {
         const int ml = g * 32 + fr;
         uint2 h;
-        h.x = (uint32_t)dequant(acc[f][g][4 * j + 0], s4.x, b4.x) |
-              ((uint32_t)dequant(acc[f][g][4 * j + 1], s4.y, b4.y) << 16);
-        h.y = (uint32_t)dequant(acc[f][g][4 * j + 2], s4.z, b4.z) |
-              ((uint32_t)dequant(acc[f][g][4 * j + 3], s4.w, b4.w) << 16);
+        h.x = (uint32_t)dequant_x<PT>(acc[f][g][4 * j + 0], sx[g], s4.x, b4.x) |
+              ((uint32_t)dequant_x<PT>(acc[f][g][4 * j + 1], sx[g], s4.y, b4.y) << 16);
+        h.y = (uint32_t)dequant_x<PT>(acc[f][g][4 * j + 2], sx[g], s4.z, b4.z) |
+              ((uint32_t)dequant_x<PT>(acc[f][g][4 * j + 3], sx[g], s4.w, b4.w) << 16);
         const int unit = (nl >> 2) ^ (ml & (kUnits - 1));
         *reinterpret_cast<uint2 *>(tile + ml * C::kTN + unit * 4) = h;
       }
@@ -317,25 +324,31 @@ __device__ __forceinline__ void prefill_body(
 
 }
 
-template <int BN, int BM, int BK, int WN, int WM, int S, int OCC>
+template <int BN, int BM, int BK, int WN, int WM, int S, int OCC, bool PT>
 __global__ __launch_bounds__(64 * WN * WM, OCC) void qgemm_prefill_kernel(
-    const int8_t *__restrict__ Xq, const int8_t *__restrict__ Wq, const float *__restrict__ sW,
-    const float *__restrict__ bp, int M, int N, int K, uint16_t *__restrict__ Y,
-    int32_t *__restrict__ acc_out, int tiles_m, int tiles_n, int group_m) {
+    const int8_t *__restrict__ Xq, const int8_t *__restrict__ Wq, const float *__restrict__ sX,
+    const float *__restrict__ sW, const float *__restrict__ bp, int M, int N, int K,
+    uint16_t *__restrict__ Y, int32_t *__restrict__ acc_out, int tiles_m, int tiles_n,
+    int group_m) {
   __shared__ __attribute__((aligned(1024)))
   int8_t smem[S * PrefillCfg<BN, BM, BK, WN, WM, S>::kStage];
-  prefill_body<BN, BM, BK, WN, WM, S>(smem, Xq, Wq, sW, bp, M, N, K, Y, acc_out, tiles_m,
-                                      tiles_n, group_m);
+  prefill_body<BN, BM, BK, WN, WM, S, PT>(smem, Xq, Wq, sX, sW, bp, M, N, K, Y, acc_out,
+                                          tiles_m, tiles_n, group_m);
 }
 
+// sX == nullptr: per-channel epilogue; else per-token scales sX [M].
 template <int BN, int BM, int BK, int WN, int WM, int S, int OCC = 1>
-hipError_t launch_prefill(const int8_t *Xq, const int8_t *Wq, const float *sW, const float *bp,
-                          int64_t M, int64_t N, int64_t K, uint16_t *Y, int32_t *acc_out,
-                          hipStream_t st, int group_m = 8) {
+hipError_t launch_prefill(const int8_t *Xq, const int8_t *Wq, const float *sX, const float *sW,
+                          const float *bp, int64_t M, int64_t N, int64_t K, uint16_t *Y,
+                          int32_t *acc_out, hipStream_t st, int group_m = 8) {
   const int tiles_m = (int)((M + BM - 1) / BM), tiles_n = (int)((N + BN - 1) / BN);
   const unsigned grid = (unsigned)(tiles_m * tiles_n);
-  qgemm_prefill_kernel<BN, BM, BK, WN, WM, S, OCC><<<grid, 64 * WN * WM, 0, st>>>(
-      Xq, Wq, sW, bp, (int)M, (int)N, (int)K, Y, acc_out, tiles_m, tiles_n, group_m);
+  if (sX)
+    qgemm_prefill_kernel<BN, BM, BK, WN, WM, S, OCC, true><<<grid, 64 * WN * WM, 0, st>>>(
+        Xq, Wq, sX, sW, bp, (int)M, (int)N, (int)K, Y, acc_out, tiles_m, tiles_n, group_m);
+  else
+    qgemm_prefill_kernel<BN, BM, BK, WN, WM, S, OCC, false><<<grid, 64 * WN * WM, 0, st>>>(
+        Xq, Wq, sX, sW, bp, (int)M, (int)N, (int)K, Y, acc_out, tiles_m, tiles_n, group_m);
   return hipGetLastError();
 }
 
@@ -345,10 +358,10 @@ using namespace detail;
 
 // One tile shape for every prefill layer: 256x256 output tiles, BK = 128,
 // 8 waves as 4 (weight rows) x 2 (tokens), a 2-stage ring (128 KiB of LDS).
-hipError_t launch_qgemm_prefill(const int8_t *Xq, const int8_t *Wq, const float *sW,
-                                const float *bprime, int64_t M, int64_t N, int64_t K,
-                                uint16_t *Y, int32_t *acc_out, hipStream_t st) {
-  return launch_prefill<256, 256, 128, 4, 2, 2>(Xq, Wq, sW, bprime, M, N, K, Y, acc_out, st);
+hipError_t launch_qgemm_prefill(const int8_t *Xq, const int8_t *Wq, const float *sX,
+                                const float *sW, const float *bprime, int64_t M, int64_t N,
+                                int64_t K, uint16_t *Y, int32_t *acc_out, hipStream_t st) {
+  return launch_prefill<256, 256, 128, 4, 2, 2>(Xq, Wq, sX, sW, bprime, M, N, K, Y, acc_out, st);
 }
 
 }  // namespace ot

@@ -7,6 +7,9 @@
 // covers 64 x 16 = 1024 consecutive channels of one row (32-byte loads and
 // 16-byte stores per lane, fully coalesced) and keeps those channels' z and
 // inv_s in registers while it walks down kRowsPerWave rows.
+//
+// Also here: the dynamic per-token quantizer of Eq. (c) for the linears that
+// the paper leaves per-token (out, fc2).
 #include "ot_common.h"
 
 namespace ot {
@@ -57,6 +60,73 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void quantize_act_kernel(
   }
 }
 
+// Per-token dynamic quantization (Eq. (c); out and fc2 inputs):
+//   s_m = fp32(max_k |x[m, k]| / qa)   (fp64 division; 1 for a zero row)
+//   Xq[m, k] = clip(rne(fp32(x[m, k]) * fp32(1 / s_m)), -qa, qa)
+// One workgroup per row: each thread holds CPT 16-byte chunks (chunks t,
+// t + T, ...) between the max reduction (exact, order-free) and the
+// quantize step, so the row is read from HBM once.
+template <int CPT, int MAXT>
+__global__ __launch_bounds__(MAXT) void quantize_per_token_kernel(
+    const uint16_t *__restrict__ x, int K, float qa, int8_t *__restrict__ Xq,
+    float *__restrict__ sX) {
+  __shared__ float red[16];
+  const int T = blockDim.x;
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6, nwaves = T >> 6;
+  const int nchunks = K / 8;
+  const int64_t row = blockIdx.x;
+  uint4 v[CPT];
+  float mx = 0.f;
+#pragma unroll
+  for (int j = 0; j < CPT; ++j) {
+    const int ch = t + j * T;
+    v[j] = ch < nchunks ? *reinterpret_cast<const uint4 *>(x + row * K + (int64_t)ch * 8)
+                        : make_uint4(0, 0, 0, 0);
+    const uint32_t w[4] = {v[j].x, v[j].y, v[j].z, v[j].w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      mx = fmaxf(mx, fabsf(half_bits_to_float((uint16_t)w[i])));
+      mx = fmaxf(mx, fabsf(half_bits_to_float((uint16_t)(w[i] >> 16))));
+    }
+  }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
+  if (lane == 0) red[wave] = mx;
+  __syncthreads();
+  mx = 0.f;
+  for (int w = 0; w < nwaves; ++w) mx = fmaxf(mx, red[w]);
+  float s = (float)((double)mx / (double)qa);
+  if (s == 0.f) s = 1.f;
+  const float inv = (float)(1.0 / (double)s);
+  if (t == 0) sX[row] = s;
+#pragma unroll
+  for (int j = 0; j < CPT; ++j) {
+    const int ch = t + j * T;
+    if (ch >= nchunks) continue;
+    const uint32_t w[4] = {v[j].x, v[j].y, v[j].z, v[j].w};
+    uint32_t packed[2] = {0, 0};
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float hv = half_bits_to_float((uint16_t)(w[e >> 1] >> (16 * (e & 1))));
+      const float u = hv * inv;  // fp32, RNE
+      const int q = (int)rintf(fminf(fmaxf(u, -qa), qa));
+      packed[e >> 2] |= (uint32_t)(q & 0xff) << (8 * (e & 3));
+    }
+    *reinterpret_cast<uint2 *>(Xq + row * K + (int64_t)ch * 8) = make_uint2(packed[0], packed[1]);
+  }
+}
+
+template <int CPT, int MAXT>
+hipError_t launch_qpt(const uint16_t *x, int64_t M, int64_t K, int qa, int8_t *Xq, float *sX,
+                      hipStream_t st) {
+  const int64_t nchunks = K / 8;
+  const int threads = (int)((nchunks + CPT * 64 - 1) / (CPT * 64)) * 64;
+  if (threads > MAXT) return hipErrorInvalidValue;
+  quantize_per_token_kernel<CPT, MAXT><<<(unsigned)M, threads, 0, st>>>(x, (int)K, (float)qa, Xq,
+                                                                        sX);
+  return hipGetLastError();
+}
+
 }  // namespace detail
 
 using namespace detail;
@@ -71,6 +141,12 @@ hipError_t launch_quantize_act(const uint16_t *x, int64_t M, int64_t K, int qa, 
   dim3 block(64, kWavesPerBlock);
   quantize_act_kernel<<<dim3(gx, (unsigned)gy), block, 0, st>>>(x, M, K, (float)qa, z, inv_s, Xq);
   return hipGetLastError();
+}
+
+hipError_t launch_quantize_act_per_token(const uint16_t *x, int64_t M, int64_t K, int qa,
+                                         int8_t *Xq, float *sX, hipStream_t st) {
+  if (K <= 4096) return launch_qpt<4, 1024>(x, M, K, qa, Xq, sX, st);
+  return launch_qpt<8, 1024>(x, M, K, qa, Xq, sX, st);
 }
 
 }  // namespace ot

@@ -53,6 +53,13 @@ def lib() -> ctypes.CDLL:
         L.ot_ln_quantize_act.restype = c_int
         L.ot_ln_quantize_act.argtypes = [vp, i64, i64, vp, vp, ctypes.c_float, c_int, vp, vp, vp,
                                          vp]
+        L.ot_quantize_act_per_token.restype = c_int
+        L.ot_quantize_act_per_token.argtypes = [vp, i64, i64, c_int, vp, vp, vp]
+        L.ot_fold_weights_per_token.restype = c_int
+        L.ot_fold_weights_per_token.argtypes = [vp, vp, vp, i64, i64, c_int, vp, vp, vp, vp]
+        L.ot_qlinear_per_token.restype = c_int
+        L.ot_qlinear_per_token.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, c_int, c_int, vp, vp,
+                                           vp, vp]
         L.ot_qlinear.restype = c_int
         L.ot_qlinear.argtypes = [vp, vp, vp, vp, i64, i64, i64, c_int, c_int, vp, vp, vp, vp]
         L.ot_qlinear_workspace_size.restype = ctypes.c_size_t
@@ -175,6 +182,50 @@ def ot_qlinear_workspace_size(M: int, N: int, K: int) -> int:
 # ---------------------------------------------------------------------------
 # Conveniences that allocate outputs with torch and call the entry points.
 # ---------------------------------------------------------------------------
+def ot_quantize_act_per_token(x, a_bits, Xq, sX, stream=None):
+    """x [M, K] fp16 -> Xq [M, K] int8 and per-token scales sX [M] fp32
+    (Eq. (c)).  Asynchronous."""
+    M, K = x.shape
+    rc = lib().ot_quantize_act_per_token(_dev(x, torch.float16, "x"), M, K, int(a_bits),
+                                         _dev(Xq, torch.int8, "Xq", (M, K)),
+                                         _dev(sX, torch.float32, "sX", (M,)), _stream(stream))
+    _check(rc, "ot_quantize_act_per_token")
+
+
+def ot_fold_weights_per_token(W, b, zres, w_bits, Wq, sW, bprime, stream=None):
+    """W [N, K] fp16, b [N] fp16 or None, zres [N] fp32 or None -> Wq, sW and
+    bprime = b + zres (Eq. (h)).  Synchronous."""
+    N, K = W.shape
+    rc = lib().ot_fold_weights_per_token(_dev(W, torch.float16, "W"),
+                                         _dev(b, torch.float16, "b", (N,)),
+                                         _dev(zres, torch.float32, "zres", (N,)), N, K,
+                                         int(w_bits), _dev(Wq, torch.int8, "Wq", (N, K)),
+                                         _dev(sW, torch.float32, "sW", (N,)),
+                                         _dev(bprime, torch.float32, "bprime", (N,)),
+                                         _stream(stream))
+    _check(rc, "ot_fold_weights_per_token")
+
+
+def ot_qlinear_per_token(Xq, Wq, sX, sW, bprime, a_bits, w_bits, Y, acc_out=None, workspace=None,
+                         stream=None):
+    """Eq. (c): Xq [M, K], Wq [N, K] int8, sX [M], sW [N], bprime [N] fp32 ->
+    Y [M, N] fp16 (and acc_out [M, N] int32 if given).  Asynchronous."""
+    M, K = Xq.shape
+    N = Wq.shape[0]
+    if Wq.shape[1] != K:
+        raise ValueError("Xq and Wq disagree on K")
+    rc = lib().ot_qlinear_per_token(_dev(Xq, torch.int8, "Xq"), _dev(Wq, torch.int8, "Wq"),
+                                    _dev(sX, torch.float32, "sX", (M,)),
+                                    _dev(sW, torch.float32, "sW", (N,)),
+                                    _dev(bprime, torch.float32, "bprime", (N,)), M, N, K,
+                                    int(a_bits), int(w_bits),
+                                    _dev(Y, torch.float16, "Y", (M, N)),
+                                    _dev(acc_out, torch.int32, "acc_out", (M, N)),
+                                    None if workspace is None else workspace.data_ptr(),
+                                    _stream(stream))
+    _check(rc, "ot_qlinear_per_token")
+
+
 def calibrate(batches, a_bits, device="cuda"):
     """Runs ot_calibrate over an iterable of fp16 [rows, K] batches (host
     numpy or device tensors).  Returns (minmax, z, s, inv_s) on the GPU."""
@@ -222,4 +273,29 @@ def qlinear(Xq, Wq, sW, bprime, a_bits, w_bits, want_acc=False):
     Y = torch.empty((M, N), dtype=torch.float16, device=Xq.device)
     acc = torch.empty((M, N), dtype=torch.int32, device=Xq.device) if want_acc else None
     ot_qlinear(Xq, Wq, sW, bprime, a_bits, w_bits, Y, acc)
+    return (Y, acc) if want_acc else Y
+
+
+def quantize_act_per_token(x, a_bits):
+    M = x.shape[0]
+    Xq = torch.empty(x.shape, dtype=torch.int8, device=x.device)
+    sX = torch.empty(M, dtype=torch.float32, device=x.device)
+    ot_quantize_act_per_token(x, a_bits, Xq, sX)
+    return Xq, sX
+
+
+def fold_weights_per_token(W, b, zres, w_bits):
+    N, K = W.shape
+    Wq = torch.empty((N, K), dtype=torch.int8, device=W.device)
+    sW = torch.empty(N, dtype=torch.float32, device=W.device)
+    bprime = torch.empty(N, dtype=torch.float32, device=W.device)
+    ot_fold_weights_per_token(W, b, zres, w_bits, Wq, sW, bprime)
+    return Wq, sW, bprime
+
+
+def qlinear_per_token(Xq, Wq, sX, sW, bprime, a_bits, w_bits, want_acc=False):
+    M, N = Xq.shape[0], Wq.shape[0]
+    Y = torch.empty((M, N), dtype=torch.float16, device=Xq.device)
+    acc = torch.empty((M, N), dtype=torch.int32, device=Xq.device) if want_acc else None
+    ot_qlinear_per_token(Xq, Wq, sX, sW, bprime, a_bits, w_bits, Y, acc)
     return (Y, acc) if want_acc else Y

@@ -90,6 +90,26 @@ def test_ln_quantize_act_argument_checks():
     assert f(16, 4, 32, 16, 16, 1e-5, 8, 16, 16, 8, NULL) == ot.OT_EINVAL  # misaligned Xq
 
 
+def test_per_token_argument_checks():
+    L = ot.lib()
+    q = L.ot_quantize_act_per_token
+    assert q(NULL, 4, 24, 8, NULL, NULL, NULL) == ot.OT_ESHAPE
+    assert q(NULL, 4, 65536 + 16, 8, NULL, NULL, NULL) == ot.OT_ESHAPE
+    assert q(NULL, 4, 32, 1, NULL, NULL, NULL) == ot.OT_EINVAL
+    assert q(NULL, 0, 32, 8, NULL, NULL, NULL) == ot.OT_OK
+    assert q(NULL, 4, 32, 8, NULL, NULL, NULL) == ot.OT_EINVAL
+    assert q(16, 4, 32, 8, 16, 8, NULL) == ot.OT_EINVAL  # misaligned sX
+    f = L.ot_fold_weights_per_token
+    assert f(NULL, NULL, NULL, 8, 32, 8, NULL, NULL, NULL, NULL) == ot.OT_EINVAL
+    assert f(16, NULL, NULL, 0, 32, 8, 16, 16, 16, NULL) == ot.OT_ESHAPE
+    assert f(16, NULL, NULL, 8, 32, 9, 16, 16, 16, NULL) == ot.OT_EINVAL
+    g = L.ot_qlinear_per_token
+    assert g(NULL, NULL, NULL, NULL, NULL, 4, 8, 24, 8, 8, NULL, NULL, NULL, NULL) == ot.OT_ESHAPE
+    assert g(NULL, NULL, NULL, NULL, NULL, 4, 8, 133152, 8, 8, NULL, NULL, NULL, NULL) == ot.OT_ERANGE
+    assert g(NULL, NULL, NULL, NULL, NULL, 0, 8, 32, 8, 8, NULL, NULL, NULL, NULL) == ot.OT_OK
+    assert g(16, 16, NULL, 16, 16, 4, 8, 32, 8, 8, 16, NULL, NULL, NULL) == ot.OT_EINVAL
+
+
 def test_calibrate_and_fold_argument_checks():
     L = ot.lib()
     assert L.ot_calibrate(NULL, 4, 32, 8, 1, NULL, NULL, NULL, NULL, NULL) == ot.OT_EINVAL
