@@ -12,7 +12,8 @@ Printed: one JSON line.  `value` is int8 TOPS over the whole step (GEMM ops
 `roofline` covers the dominant kernel (the prefill GEMM) with its duration
 measured by HIP events around each launch inside the timed region; the
 decode regime (OPT-30B shapes, M in {1, 8, 32, 64}) is reported under
-`decode` in GB/s against HBM; `ln_quantize` times the LayerNorm fused with
+`decode` in GB/s against HBM; `mixed_block` times the paper's own split
+(per-channel qkv/fc1, per-token out/fc2); `ln_quantize` times the LayerNorm fused with
 symmetrization and quantization (qkv and fc1 inputs) against torch's
 LayerNorm plus ot_quantize_act; `fp16_baseline` times torch's fp16 linear on
 the same shapes; `cpu_baseline` times the CPU oracle on a bounded sample.
@@ -49,6 +50,8 @@ def parse():
     p.add_argument("--no-fp16", action="store_true", help="skip the fp16 torch baseline")
     p.add_argument("--no-cpu", action="store_true", help="skip the CPU-oracle baseline")
     p.add_argument("--no-ln", action="store_true", help="skip the fused LayerNorm report")
+    p.add_argument("--no-mixed", action="store_true",
+                   help="skip the per-channel + per-token block report")
     p.add_argument("--iters", type=int, default=50, help="iterations for the side measurements")
     p.add_argument("--copy-probe", action="store_true",
                    help="only run a plain 1 GiB device copy (calibrates the HBM byte counters)")
@@ -157,6 +160,44 @@ def ln_quantize_report(torch, ot, synth, wl, iters):
             f"{umed * 1e3:.1f} us")
         del h, calib, Xq, Xq2
     return out
+
+
+def mixed_block_report(torch, ot, wl, layers, iters):
+    """The paper's own split (Sec. 3.2, Sec. 4.1): qkv and fc1 (LayerNorm
+    outputs) on the static per-channel path, out and fc2 on the dynamic
+    per-token path of Eq. (c).  Same shapes and inputs as the main step;
+    the per-token weights are folded (untimed) from the same fp16 weights."""
+    M = wl.M
+    plan = []
+    for L in layers:
+        if L["name"] in ("out", "fc2"):
+            Wq, sW, bp = ot.fold_weights_per_token(L["W16"], L["b16"], None, wl.w_bits)
+            Xq = torch.empty((M, L["K"]), dtype=torch.int8, device="cuda")
+            sX = torch.empty(M, dtype=torch.float32, device="cuda")
+            plan.append(("token", L, Wq, sW, bp, Xq, sX))
+        else:
+            plan.append(("channel", L, L["Wq"], L["sW"], L["bp"], L["Xq"], None))
+
+    def step():
+        for kind, L, Wq, sW, bp, Xq, sX in plan:
+            if kind == "token":
+                ot.ot_quantize_act_per_token(L["X"], wl.a_bits, Xq, sX)
+                ot.ot_qlinear_per_token(Xq, Wq, sX, sW, bp, wl.a_bits, wl.w_bits, L["Y"])
+            else:
+                ot.ot_quantize_act(L["X"], wl.a_bits, L["z"], L["inv_s"], Xq)
+                ot.ot_qlinear(Xq, Wq, sW, bp, wl.a_bits, wl.w_bits, L["Y"])
+    med, p10, p90 = median_ms(torch, step, iters)
+    ops = sum(2.0 * M * L["N"] * L["K"] for L in layers)
+    # the per-token quantizer alone, on fc2's input
+    kind, L, Wq, sW, bp, Xq, sX = plan[3]
+    qmed, _, _ = median_ms(torch, lambda: ot.ot_quantize_act_per_token(L["X"], wl.a_bits, Xq, sX),
+                           iters)
+    qbytes = 3 * M * L["K"] + 4 * M
+    log(f"mixed block (per-channel qkv/fc1, per-token out/fc2): {med:.3f} ms "
+        f"({ops / (med * 1e-3) / 1e12:.0f} TOPS); per-token quantize fc2 {qmed * 1e3:.1f} us")
+    return dict(ms_per_step=med, p10_ms=p10, p90_ms=p90, tops=ops / (med * 1e-3) / 1e12,
+                per_token_quantize_fc2_us=qmed * 1e3,
+                per_token_quantize_fc2_GBps=qbytes / (qmed * 1e-3) / 1e9)
 
 
 def decode_report(torch, ot, synth, wl, pool, iters, with_fp16):
@@ -320,7 +361,7 @@ def traffic_record(d, workload):
                               "bytes": (f * factors["FETCH_SIZE"] + w * factors["WRITE_SIZE"]) * 1024}
         alg[L.name] = wl.M * L.K + L.N * L.K + 2 * wl.M * L.N + 8 * L.N
     cmd = "cd /tmp && timeout -s KILL 120 rocprofv3 --pmc {c} --output-format csv -d <out>/{sub} -o p -- python -u <repo>/bench.py {args}"
-    bench_args = "--steps 2 --warmup 1 --no-cpu --no-fp16 --no-decode --no-ln"
+    bench_args = "--steps 2 --warmup 1 --no-cpu --no-fp16 --no-decode --no-ln --no-mixed"
     rec = {
         "kernel": "qgemm_prefill_kernel<256,256,128,4,2,2,1>",
         "workload": f"{wl.name} ({wl.M} tokens; " + ", ".join(L.name for L in wl.layers) + ")",
@@ -482,6 +523,8 @@ def main():
                                     sum(L["K"] * L["N"] + 8 * L["N"] for L in layers))
         result["fp16_baseline"] = fb
         log(f"fp16 linear stack {fb['ms_per_stack']:.3f} ms ({fb['tflops']:.0f} TFLOPs)")
+    if not args.no_mixed:
+        result["mixed_block"] = mixed_block_report(torch, ot, wl, layers, args.iters)
     if not args.no_cpu:
         from oracle import ot_oracle
         result["cpu_baseline"] = cpu_baseline(ot_oracle, layers, M)
