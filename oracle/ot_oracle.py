@@ -19,6 +19,8 @@ Functions and the passages they follow
 --------------------------------------
 calibrate       Sec. 3.2 (symmetrization factor z from per-channel max/min)
                 and App. A (static min-max calibration of activations).
+scales_from_minmax  the same scales from a stored calibration state, for
+                another bit-width or without symmetrization (Sec. 4.4).
 fold_weights    Sec. 3.1, Eq. (e) (W_s = W scaled by s^X along input
                 channels), Eq. (f) (per-output-channel quantization of W_s),
                 Sec. 3.2, Eq. (g) (shift z moved into the bias: z W^T + b),
@@ -123,6 +125,31 @@ def calibrate(batches, a_bits: int):
     inv_s = (1.0 / s.astype(np.float64)).astype(np.float32)
     minmax = np.concatenate([lo, hi]).astype(np.float32)
     return minmax, z, s, inv_s
+
+
+def scales_from_minmax(minmax, a_bits: int, symmetrize: bool = True):
+    """(z, s, inv_s) from a calibration state minmax [2K] (the K minima then
+    the K maxima, as calibrate returns it), for ``a_bits`` codes.
+
+    With symmetrization (Sec. 3.2) this is calibrate's rule: z = (hi + lo)/2,
+    s = ((hi - lo)/2)/qa.  Without it (the ablation of Sec. 4.4, Table 6)
+    the range is not shifted: z = 0 and s = max(|lo|, |hi|)/qa, so the
+    larger side of the range lands on +-qa and the other side wastes codes.
+    float64 math, float32 storage; s = 1 where it would be 0.
+    """
+    qa = qmax(a_bits)
+    mm = np.asarray(minmax, dtype=np.float32).astype(np.float64)
+    K = mm.size // 2
+    lo, hi = mm[:K], mm[K:]
+    if symmetrize:
+        z = ((hi + lo) / 2.0).astype(np.float32)
+        s = (((hi - lo) / 2.0) / float(qa)).astype(np.float32)
+    else:
+        z = np.zeros(K, dtype=np.float32)
+        s = (np.maximum(np.abs(lo), np.abs(hi)) / float(qa)).astype(np.float32)
+    s[s == 0] = np.float32(1.0)
+    inv_s = (1.0 / s.astype(np.float64)).astype(np.float32)
+    return z, s, inv_s
 
 
 # --------------------------------------------------------------------------
