@@ -55,6 +55,9 @@ def parse():
     p.add_argument("--iters", type=int, default=50, help="iterations for the side measurements")
     p.add_argument("--copy-probe", action="store_true",
                    help="only run a plain 1 GiB device copy (calibrates the HBM byte counters)")
+    p.add_argument("--quality", action="store_true",
+                   help="only run the symmetrization ablation / bit-width sweep of output error "
+                        "against float64 (one JSON line)")
     p.add_argument("--traffic-record", metavar="DIR",
                    help="host only: write the prefill GEMM's HBM traffic record from the "
                         "rocprofv3 counter runs under DIR (fetch/, write/, copy_fetch/, copy_write/)")
@@ -444,6 +447,12 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     if args.copy_probe:
         copy_probe(torch)
+        return
+    if args.quality:
+        from paper_2406_18832_amd import quality
+        ot.lib()
+        recs = quality.sweep(log=log)
+        print(json.dumps({"quality_sweep": recs}), flush=True)
         return
     ot.lib()
     wl = synth.WORKLOADS[args.workload]

@@ -83,6 +83,23 @@ ot_status ot_calibrate(const uint16_t *x, int64_t rows, int64_t K, int a_bits,
                        float *inv_s, void *stream);
 
 /*
+ * ot_scales_from_minmax -- z, s, 1/s from a calibration state (the minmax
+ * that ot_calibrate keeps), for any bit-width, with or without the
+ * symmetrization of Sec. 3.2 (the ablation of Sec. 4.4, Table 6):
+ *   symmetrize != 0:  z_k = (hi_k + lo_k)/2,  s_k = ((hi_k - lo_k)/2)/qa
+ *   symmetrize == 0:  z_k = 0,                s_k = max(|lo_k|, |hi_k|)/qa
+ * fp64 math, fp32 storage, s_k = 1 where it would be 0, inv_s_k =
+ * fp32(1/s_k).  With symmetrize != 0 and the calibration's own a_bits this
+ * reproduces ot_calibrate's outputs exactly.
+ *   minmax [2K] fp32 (device; the K minima then the K maxima, finite).
+ *   z, s, inv_s [K] fp32 outputs (device).
+ * Asynchronous on stream.
+ */
+ot_status ot_scales_from_minmax(const float *minmax, int64_t K, int a_bits,
+                                int symmetrize, float *z, float *s,
+                                float *inv_s, void *stream);
+
+/*
  * ot_fold_weights -- the offline weight and bias transform.
  * Sec. 3.1 Eq. (e) (W_s = W scaled by s along the input channels), Eq. (f)
  * (per-output-channel quantization of W_s), Sec. 3.2 Eq. (g) (the shift z

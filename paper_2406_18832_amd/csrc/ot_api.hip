@@ -61,10 +61,19 @@ ot_status ot_calibrate(const uint16_t *x, int64_t rows, int64_t K, int a_bits, i
     return rc;
   if ((rc = hip_status(hipStreamSynchronize(st))) != OT_OK) return rc;
   if (!all_finite(state)) return OT_ENONFINITE;
-  if ((rc = hip_status(ot::launch_calib_finalize(minmax, K, qmax(a_bits), z, s, inv_s, st))) !=
+  if ((rc = hip_status(ot::launch_calib_finalize(minmax, K, qmax(a_bits), 1, z, s, inv_s, st))) !=
       OT_OK)
     return rc;
   return hip_status(hipStreamSynchronize(st));
+}
+
+ot_status ot_scales_from_minmax(const float *minmax, int64_t K, int a_bits, int symmetrize,
+                                float *z, float *s, float *inv_s, void *stream) {
+  if (!bits_ok(a_bits) || K < 0) return OT_EINVAL;
+  if (K == 0 || K > kMaxRows) return OT_ESHAPE;
+  if (!minmax || !z || !s || !inv_s) return OT_EINVAL;
+  return hip_status(ot::launch_calib_finalize(minmax, K, qmax(a_bits), symmetrize ? 1 : 0, z, s,
+                                              inv_s, static_cast<hipStream_t>(stream)));
 }
 
 // Reads sW and b' back (synchronously): a NaN scale marks non-finite weights,

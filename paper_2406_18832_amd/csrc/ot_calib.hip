@@ -76,8 +76,11 @@ __global__ __launch_bounds__(kThreads) void calib_minmax_kernel(const uint16_t *
 }
 
 // z, s, inv_s from the state, in fp64 with one rounding to fp32 each.
+// symmetrize != 0: Sec. 3.2's z = (hi + lo) / 2, s = ((hi - lo) / 2) / qa.
+// symmetrize == 0 (the ablation of Sec. 4.4): z = 0, s = max(|lo|, |hi|) / qa.
 __global__ __launch_bounds__(kThreads) void calib_finalize_kernel(const float *__restrict__ minmax,
                                                                   int64_t K, int qa,
+                                                                  int symmetrize,
                                                                   float *__restrict__ z,
                                                                   float *__restrict__ s,
                                                                   float *__restrict__ inv_s) {
@@ -85,10 +88,11 @@ __global__ __launch_bounds__(kThreads) void calib_finalize_kernel(const float *_
   if (k >= K) return;
   const double lo = (double)minmax[k];
   const double hi = (double)minmax[K + k];
-  const double half = (hi - lo) / 2.0;  // exact: both are fp16 values
+  // exact: both are fp16 values
+  const double half = symmetrize ? (hi - lo) / 2.0 : fmax(fabs(lo), fabs(hi));
   float sk = (float)(half / (double)qa);
   if (sk == 0.0f) sk = 1.0f;
-  z[k] = (float)((hi + lo) / 2.0);
+  z[k] = symmetrize ? (float)((hi + lo) / 2.0) : 0.0f;
   s[k] = sk;
   inv_s[k] = (float)(1.0 / (double)sk);
 }
@@ -112,9 +116,10 @@ hipError_t launch_calib_minmax(const uint16_t *x, int64_t rows, int64_t K, float
   return hipGetLastError();
 }
 
-hipError_t launch_calib_finalize(const float *minmax, int64_t K, int qa, float *z, float *s,
-                                 float *inv_s, hipStream_t st) {
-  calib_finalize_kernel<<<blocks_for(K, kThreads), kThreads, 0, st>>>(minmax, K, qa, z, s, inv_s);
+hipError_t launch_calib_finalize(const float *minmax, int64_t K, int qa, int symmetrize, float *z,
+                                 float *s, float *inv_s, hipStream_t st) {
+  calib_finalize_kernel<<<blocks_for(K, kThreads), kThreads, 0, st>>>(minmax, K, qa, symmetrize, z,
+                                                                      s, inv_s);
   return hipGetLastError();
 }
 

@@ -39,8 +39,8 @@ __device__ inline uint16_t float_to_half_bits(float f) {
 hipError_t launch_calib_reset(float *minmax, int64_t K, hipStream_t st);
 hipError_t launch_calib_minmax(const uint16_t *x, int64_t rows, int64_t K, float *minmax,
                                hipStream_t st);
-hipError_t launch_calib_finalize(const float *minmax, int64_t K, int qa, float *z, float *s,
-                                 float *inv_s, hipStream_t st);
+hipError_t launch_calib_finalize(const float *minmax, int64_t K, int qa, int symmetrize, float *z,
+                                 float *s, float *inv_s, hipStream_t st);
 hipError_t launch_fold(const uint16_t *W, const uint16_t *b, int64_t N, int64_t K, int qw,
                        const float *z, const float *s, int8_t *Wq, float *sW, float *bprime,
                        hipStream_t st);

@@ -60,6 +60,8 @@ def lib() -> ctypes.CDLL:
         L.ot_qlinear_per_token.restype = c_int
         L.ot_qlinear_per_token.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, c_int, c_int, vp, vp,
                                            vp, vp]
+        L.ot_scales_from_minmax.restype = c_int
+        L.ot_scales_from_minmax.argtypes = [vp, i64, c_int, c_int, vp, vp, vp, vp]
         L.ot_qlinear.restype = c_int
         L.ot_qlinear.argtypes = [vp, vp, vp, vp, i64, i64, i64, c_int, c_int, vp, vp, vp, vp]
         L.ot_qlinear_workspace_size.restype = ctypes.c_size_t
@@ -182,6 +184,25 @@ def ot_qlinear_workspace_size(M: int, N: int, K: int) -> int:
 # ---------------------------------------------------------------------------
 # Conveniences that allocate outputs with torch and call the entry points.
 # ---------------------------------------------------------------------------
+def ot_scales_from_minmax(minmax, a_bits, symmetrize, z, s, inv_s, stream=None):
+    """minmax [2K] fp32 -> z, s, inv_s [K] fp32 for a_bits, with or without
+    symmetrization.  Asynchronous."""
+    K = minmax.shape[0] // 2
+    rc = lib().ot_scales_from_minmax(_dev(minmax, torch.float32, "minmax", (2 * K,)), K,
+                                     int(a_bits), 1 if symmetrize else 0,
+                                     _dev(z, torch.float32, "z", (K,)),
+                                     _dev(s, torch.float32, "s", (K,)),
+                                     _dev(inv_s, torch.float32, "inv_s", (K,)), _stream(stream))
+    _check(rc, "ot_scales_from_minmax")
+
+
+def scales_from_minmax(minmax, a_bits, symmetrize=True):
+    K = minmax.shape[0] // 2
+    z, s, inv_s = (torch.empty(K, dtype=torch.float32, device=minmax.device) for _ in range(3))
+    ot_scales_from_minmax(minmax, a_bits, symmetrize, z, s, inv_s)
+    return z, s, inv_s
+
+
 def ot_quantize_act_per_token(x, a_bits, Xq, sX, stream=None):
     """x [M, K] fp16 -> Xq [M, K] int8 and per-token scales sX [M] fp32
     (Eq. (c)).  Asynchronous."""
