@@ -44,6 +44,11 @@ fold_weights_per_token  Eq. (c) and Eq. (h): per-output-channel weight
                 scales without an activation scale, and the bias b + z that
                 carries a symmetrized residual stream back (Eq. (h)).
 epilogue_per_token      Eq. (c): s^X_m s^W_n times the integer sum, plus b'.
+fold_weights_asym       the "Int8" weight setting (Sec. 4.1, App. A):
+                per-output-channel asymmetric quantization of W_s with a zero
+                point, Eq. (a) with z != 0.
+int_gemm_asym   Eq. (f)'s integer sum with the weight zero point removed:
+                sum_k Xq (Wq - zW).
 reference_fp64, folded_fp64     exact-arithmetic references (tests only).
 
 Readings taken where the paper is silent (each applies to both this oracle
@@ -455,6 +460,65 @@ def epilogue_per_token(acc, sX, sW, bprime):
     y = p + np.asarray(bprime, dtype=np.float32)[None, :]
     assert y.dtype == np.float32
     return y.astype(np.float16)
+
+
+# --------------------------------------------------------------------------
+# Asymmetric per-channel weights, the paper's "Int8" setting (Sec. 4.1,
+# App. A), with Eq. (a)'s zero point
+# --------------------------------------------------------------------------
+def fold_weights_asym(W, b, z, s, w_bits: int):
+    """Fold s into W (Eq. (e)) and quantize each output channel of W_s
+    asymmetrically, Eq. (a): codes c = clip(round(W_s / sW) + zW, 0, L),
+    L = 2^bits - 1, dequantized as (c - zW) sW.
+
+      lo_n, hi_n = min(min_k W_s[n, k], 0), max(max_k W_s[n, k], 0)
+                   (the range always holds 0, so 0 is represented exactly)
+      sW_n = fp32((hi_n - lo_n) / L)        (float64; 1 where it is 0)
+      zW_n = clip(round(-lo_n / sW_n), 0, L)
+    Codes are stored signed, shifted by 2^(bits-1) so that they fit int8 for
+    the int8 matrix cores: Wq = c - 2^(bits-1), zWq = zW - 2^(bits-1).  The
+    bias b' = z W^T + b is the symmetric path's (original W, Eq. (g)).
+    Returns (Wq int8 [N, K], sW float32 [N], zWq int32 [N], b' float32 [N]).
+    """
+    L = (1 << int(w_bits)) - 1
+    half = 1 << (int(w_bits) - 1)
+    qmax(w_bits)  # validates the bit-width
+    W = np.asarray(W)
+    if W.dtype != np.float16 or W.ndim != 2:
+        raise ValueError("W must be fp16 [N, K]")
+    N, K = W.shape
+    W64 = W.astype(np.float64)
+    b64 = np.zeros(N) if b is None else np.asarray(b).astype(np.float64)
+    if not (np.all(np.isfinite(W64)) and np.all(np.isfinite(b64))):
+        raise NonFinite("non-finite weights or bias")
+    s64 = np.asarray(s, dtype=np.float32).astype(np.float64)
+    z64 = np.asarray(z, dtype=np.float32).astype(np.float64)
+    Ws = W64 * s64[None, :]
+    lo = np.minimum(Ws.min(axis=1), 0.0)
+    hi = np.maximum(Ws.max(axis=1), 0.0)
+    sW = ((hi - lo) / float(L)).astype(np.float32)
+    sW[sW == 0] = np.float32(1.0)
+    sW64 = sW.astype(np.float64)
+    zW = np.clip(np.rint(-lo / sW64), 0, L)
+    c = np.clip(np.rint(Ws / sW64[:, None]) + zW[:, None], 0, L)
+    Wq = (c - half).astype(np.int8)
+    zWq = (zW - half).astype(np.int32)
+    acc = np.zeros(N)
+    for k in range(K):
+        acc = acc + z64[k] * W64[:, k]
+    bprime = (acc + b64).astype(np.float32)
+    return Wq, sW, zWq, bprime
+
+
+def int_gemm_asym(Xq, Wq, zWq):
+    """acc[m, n] = sum_k Xq[m, k] (Wq[n, k] - zWq[n]), exact (float64 BLAS on
+    integers below 2^53), as int32.  The shift of the stored codes cancels:
+    Wq - zWq = c - zW."""
+    Xq = np.asarray(Xq)
+    Wd = np.asarray(Wq).astype(np.int64) - np.asarray(zWq, dtype=np.int64)[:, None]
+    acc = Xq.astype(np.float64) @ Wd.astype(np.float64).T
+    assert np.all(np.abs(acc) < INT32_LIMIT)
+    return acc.astype(np.int32)
 
 
 def pipeline(X, W, b, calib_batches, a_bits: int, w_bits: int):
