@@ -201,6 +201,39 @@ ot_status ot_qlinear(const int8_t *Xq, const int8_t *Wq, const float *sW,
                      void *workspace, void *stream);
 
 /*
+ * Asymmetric weights, the paper's "Int8" setting (Sec. 4.1, App. A):
+ * per-output-channel asymmetric quantization of W_s = W diag(s), Eq. (a)
+ * with a zero point.  With L = 2^w_bits - 1, per output channel n:
+ *   lo, hi = min(min_k W_s[n,k], 0), max(max_k W_s[n,k], 0)
+ *   sW[n]  = fp32((hi - lo) / L)  (1 where 0);  zp = clip(rne(-lo/sW), 0, L)
+ *   c[n,k] = clip(rne(W_s[n,k] / sW[n]) + zp, 0, L)   (fp64, correctly rounded)
+ * stored shifted so that they fit int8: Wq = c - 2^(w_bits-1),
+ * zW[n] = zp - 2^(w_bits-1).  bprime as for ot_fold_weights.
+ *
+ * ot_fold_weights_asym -- arguments as ot_fold_weights plus zW [N] int32
+ * output.  Synchronous; OT_ENONFINITE as ot_fold_weights.
+ */
+ot_status ot_fold_weights_asym(const uint16_t *W, const uint16_t *b, int64_t N,
+                               int64_t K, int w_bits, const float *z,
+                               const float *s, int8_t *Wq, float *sW,
+                               int32_t *zW, float *bprime, void *stream);
+
+/*
+ * ot_qlinear_asym -- the quantized linear with asymmetric weights:
+ *   acc[m,n] = sum_k Xq[m,k] (Wq[n,k] - zW[n])   exact in int32
+ *   Y[m,n]   = fp16(fp32(fp32(acc[m,n]) * sW[n]) + bprime[n])
+ * The kernels compute sum_k Xq Wq and subtract zW[n] times the token's code
+ * sum, which they take from the token fragments they already hold.
+ * Arguments as ot_qlinear plus zW [N] int32 (device); acc_out receives acc.
+ * OT_ERANGE when K * qa * 2^w_bits >= 2^31.
+ */
+ot_status ot_qlinear_asym(const int8_t *Xq, const int8_t *Wq, const float *sW,
+                          const int32_t *zW, const float *bprime, int64_t M,
+                          int64_t N, int64_t K, int a_bits, int w_bits,
+                          uint16_t *Y, int32_t *acc_out, void *workspace,
+                          void *stream);
+
+/*
  * Per-token path.  The paper keeps the linears without activation outliers
  * (out and fc2, whose inputs are not LayerNorm outputs) on per-token
  * symmetric activation quantization, Eq. (c), and carries a symmetrized

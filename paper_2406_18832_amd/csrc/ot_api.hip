@@ -145,7 +145,7 @@ ot_status ot_qlinear(const int8_t *Xq, const int8_t *Wq, const float *sW, const 
   if (!aligned16(Xq) || !aligned16(Wq) || !aligned16(sW) || !aligned16(bprime) || !aligned16(Y) ||
       (acc_out && !aligned16(acc_out)))
     return OT_EINVAL;
-  return hip_status(ot::launch_qgemm(Xq, Wq, nullptr, sW, bprime, M, N, K, Y, acc_out,
+  return hip_status(ot::launch_qgemm(Xq, Wq, nullptr, nullptr, sW, bprime, M, N, K, Y, acc_out,
                                      static_cast<hipStream_t>(stream)));
 }
 
@@ -189,7 +189,42 @@ ot_status ot_qlinear_per_token(const int8_t *Xq, const int8_t *Wq, const float *
   if (!aligned16(Xq) || !aligned16(Wq) || !aligned16(sW) || !aligned16(bprime) || !aligned16(Y) ||
       (acc_out && !aligned16(acc_out)))
     return OT_EINVAL;
-  return hip_status(ot::launch_qgemm(Xq, Wq, sX, sW, bprime, M, N, K, Y, acc_out,
+  return hip_status(ot::launch_qgemm(Xq, Wq, sX, nullptr, sW, bprime, M, N, K, Y, acc_out,
+                                     static_cast<hipStream_t>(stream)));
+}
+
+ot_status ot_fold_weights_asym(const uint16_t *W, const uint16_t *b, int64_t N, int64_t K,
+                               int w_bits, const float *z, const float *s, int8_t *Wq, float *sW,
+                               int32_t *zW, float *bprime, void *stream) {
+  if (!W || !z || !s || !Wq || !sW || !zW || !bprime) return OT_EINVAL;
+  if (!bits_ok(w_bits) || N < 0 || K < 0) return OT_EINVAL;
+  if (N == 0 || K == 0 || N > kMaxRows || K > kMaxRows) return OT_ESHAPE;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  ot_status rc;
+  if ((rc = hip_status(ot::launch_fold_asym(W, b, N, K, w_bits, z, s, Wq, sW, zW, bprime, st))) !=
+      OT_OK)
+    return rc;
+  return fold_outputs_finite(sW, bprime, N, st);
+}
+
+ot_status ot_qlinear_asym(const int8_t *Xq, const int8_t *Wq, const float *sW, const int32_t *zW,
+                          const float *bprime, int64_t M, int64_t N, int64_t K, int a_bits,
+                          int w_bits, uint16_t *Y, int32_t *acc_out, void *workspace,
+                          void *stream) {
+  (void)workspace;
+  if (!bits_ok(a_bits) || !bits_ok(w_bits) || M < 0 || N < 0 || K < 0) return OT_EINVAL;
+  if (N == 0 || K < 16 || K % 16 != 0 || K > kMaxK || M > kMaxRows || N > kMaxRows)
+    return OT_ESHAPE;
+  if ((M + 255) / 256 * ((N + 255) / 256) > kMaxRows) return OT_ESHAPE;
+  // |Xq| <= qa against stored codes and zero points of magnitude <= 2^(w_bits-1):
+  // every partial sum stays below K qa 2^w_bits
+  if (K * qmax(a_bits) * (int64_t(1) << w_bits) >= (int64_t(1) << 31)) return OT_ERANGE;
+  if (M == 0) return OT_OK;
+  if (!Xq || !Wq || !sW || !zW || !bprime || !Y) return OT_EINVAL;
+  if (!aligned16(Xq) || !aligned16(Wq) || !aligned16(sW) || !aligned16(zW) ||
+      !aligned16(bprime) || !aligned16(Y) || (acc_out && !aligned16(acc_out)))
+    return OT_EINVAL;
+  return hip_status(ot::launch_qgemm(Xq, Wq, nullptr, zW, sW, bprime, M, N, K, Y, acc_out,
                                      static_cast<hipStream_t>(stream)));
 }
 

@@ -50,15 +50,21 @@ hipError_t launch_ln_quantize_act(const uint16_t *h, int64_t M, int64_t K, const
                                   const uint16_t *beta, float eps, int qa, const float *z,
                                   const float *inv_s, int8_t *Xq, hipStream_t st);
 hipError_t launch_qgemm_decode(const int8_t *Xq, const int8_t *Wq, const float *sX,
-                               const float *sW, const float *bprime, int64_t M, int64_t N,
-                               int64_t K, uint16_t *Y, int32_t *acc_out, hipStream_t st);
+                               const int32_t *zW, const float *sW, const float *bprime,
+                               int64_t M, int64_t N, int64_t K, uint16_t *Y, int32_t *acc_out,
+                               hipStream_t st);
 hipError_t launch_qgemm_prefill(const int8_t *Xq, const int8_t *Wq, const float *sX,
-                                const float *sW, const float *bprime, int64_t M, int64_t N,
-                                int64_t K, uint16_t *Y, int32_t *acc_out, hipStream_t st);
-// sX == nullptr: per-channel epilogue (Eq. (g)); else per-token scales (Eq. (c)).
-hipError_t launch_qgemm(const int8_t *Xq, const int8_t *Wq, const float *sX, const float *sW,
-                        const float *bprime, int64_t M, int64_t N, int64_t K, uint16_t *Y,
-                        int32_t *acc_out, hipStream_t st);
+                                const int32_t *zW, const float *sW, const float *bprime,
+                                int64_t M, int64_t N, int64_t K, uint16_t *Y, int32_t *acc_out,
+                                hipStream_t st);
+// Epilogue: sX != nullptr per-token scales (Eq. (c)); zW != nullptr
+// asymmetric weight zero points (Eq. (a)); neither, per-channel (Eq. (g)).
+hipError_t launch_qgemm(const int8_t *Xq, const int8_t *Wq, const float *sX, const int32_t *zW,
+                        const float *sW, const float *bprime, int64_t M, int64_t N, int64_t K,
+                        uint16_t *Y, int32_t *acc_out, hipStream_t st);
+hipError_t launch_fold_asym(const uint16_t *W, const uint16_t *b, int64_t N, int64_t K,
+                            int w_bits, const float *z, const float *s, int8_t *Wq, float *sW,
+                            int32_t *zW, float *bprime, hipStream_t st);
 hipError_t launch_quantize_act_per_token(const uint16_t *x, int64_t M, int64_t K, int qa,
                                          int8_t *Xq, float *sX, hipStream_t st);
 hipError_t launch_fold_per_token(const uint16_t *W, const uint16_t *b, const float *zres,

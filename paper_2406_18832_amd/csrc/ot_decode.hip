@@ -37,7 +37,8 @@ struct DecodeCfg {
   static_assert(kLoads >= 1 && kLoads * 1024 * kWaves == kStage, "stage splits evenly over the waves");
   static_assert(kTokRows % kRowsPerLoad == 0, "a load never straddles tokens and weights");
   static_assert((S - 2) * kLoads <= 63 && S >= 2, "vmcnt range");
-  static_assert(kRed <= S * kStage, "partial sums fit in the ring");
+  static constexpr int kRedRs = (NK - 1) * MB * 64 * 4;  // token code sums, bytes
+  static_assert(kRed + kRedRs <= S * kStage, "partial sums fit in the ring");
 };
 
 // cache-policy operand of a buffer load on gfx950: non-temporal
@@ -49,11 +50,12 @@ __device__ __forceinline__ int swz_rows(int r) {
   else return r & 15;
 }
 
-template <int MB, int NR, int NK, int RBW, int BKD, int S, bool PT>
+template <int MB, int NR, int NK, int RBW, int BKD, int S, int EPI>
 __device__ __forceinline__ void decode_body(
     int8_t *smem, const int8_t *__restrict__ Xq, const int8_t *__restrict__ Wq,
-    const float *__restrict__ sX, const float *__restrict__ sW, const float *__restrict__ bp,
-    int M, int N, int K, uint16_t *__restrict__ Y, int32_t *__restrict__ acc_out) {
+    const float *__restrict__ sX, const int32_t *__restrict__ zW, const float *__restrict__ sW,
+    const float *__restrict__ bp, int M, int N, int K, uint16_t *__restrict__ Y,
+    int32_t *__restrict__ acc_out) {
   using C = DecodeCfg<MB, NR, NK, RBW, BKD, S>;
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -118,6 +120,9 @@ __device__ __forceinline__ void decode_body(
   for (int i = 0; i < RBW; ++i)
 #pragma unroll
     for (int j = 0; j < MB; ++j) acc[i][j] = v4i{};
+  int rs[MB];
+#pragma unroll
+  for (int j = 0; j < MB; ++j) rs[j] = 0;
 
 #pragma unroll
   for (int t = 0; t < S - 1; ++t) issue(t);
@@ -138,6 +143,10 @@ __device__ __forceinline__ void decode_body(
 #pragma unroll
         for (int j = 0; j < MB; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(wf[i], xf[j], acc[i][j], 0, 0, 0);
+      if constexpr (EPI == kEpiAsym) {
+#pragma unroll
+        for (int j = 0; j < MB; ++j) rs[j] = byte_sum16(xf[j], rs[j]);
+      }
     }
     // stage st+1 has landed once at most S-2 younger stages are in flight;
     // after the barrier every wave is done with stage st, whose slot takes st+S
@@ -149,65 +158,90 @@ __device__ __forceinline__ void decode_body(
   // the ring's last (zero-filling) loads must land before its bytes are reused
   wait_vmcnt<0>();
 
+  // asymmetric weights: token code sums over this wave's K slice (the four
+  // 16-lane groups hold the four 16-byte parts of every 64-byte step)
+  if constexpr (EPI == kEpiAsym) {
+#pragma unroll
+    for (int j = 0; j < MB; ++j) {
+      rs[j] += __shfl_xor(rs[j], 16);
+      rs[j] += __shfl_xor(rs[j], 32);
+    }
+  }
+
   if constexpr (NK > 1) {
     lds_barrier();
     v4i *red = reinterpret_cast<v4i *>(smem);
+    int *red_rs = reinterpret_cast<int *>(smem + C::kRed);  // [NK-1][MB][64]
     if (kg > 0) {
 #pragma unroll
       for (int i = 0; i < RBW; ++i)
 #pragma unroll
         for (int j = 0; j < MB; ++j)
           red[((((kg - 1) * NR + rg) * RBW + i) * MB + j) * 64 + lane] = acc[i][j];
+      if (EPI == kEpiAsym && rg == 0) {
+#pragma unroll
+        for (int j = 0; j < MB; ++j) red_rs[((kg - 1) * MB + j) * 64 + lane] = rs[j];
+      }
     }
     __builtin_amdgcn_s_waitcnt(0xC07F);
     lds_barrier();
     if (kg > 0) return;
 #pragma unroll
-    for (int g = 0; g < NK - 1; ++g)
+    for (int g = 0; g < NK - 1; ++g) {
 #pragma unroll
       for (int i = 0; i < RBW; ++i)
 #pragma unroll
         for (int j = 0; j < MB; ++j)
           acc[i][j] += red[(((g * NR + rg) * RBW + i) * MB + j) * 64 + lane];
+      if constexpr (EPI == kEpiAsym) {
+#pragma unroll
+        for (int j = 0; j < MB; ++j) rs[j] += red_rs[(g * MB + j) * 64 + lane];
+      }
+    }
   }
 
   // 16x16 output blocks: lane l holds token l%16 and channels 4*(l/16) + r
 #pragma unroll
   for (int j = 0; j < MB; ++j) {
     const int m = j * 16 + r16;
-    const float sx = (PT && m < M) ? sX[m] : 0.f;
+    const float sx = (EPI == kEpiToken && m < M) ? sX[m] : 0.f;
 #pragma unroll
     for (int i = 0; i < RBW; ++i) {
       const int64_t n = nwg0 + (rg * RBW + i) * 16 + 4 * c4;
-      store4<PT>(Y, acc_out, sW, bp, sx, m, n, M, N, acc[i][j][0], acc[i][j][1], acc[i][j][2],
-                 acc[i][j][3]);
+      store4<EPI>(Y, acc_out, sW, bp, zW, sx, rs[j], m, n, M, N, acc[i][j][0], acc[i][j][1],
+                  acc[i][j][2], acc[i][j][3]);
     }
   }
 }
 
-template <int MB, int NR, int NK, int RBW, int BKD, int S, bool PT>
+template <int MB, int NR, int NK, int RBW, int BKD, int S, int EPI>
 __global__ __launch_bounds__(64 * NR * NK) void qgemm_decode_kernel(
     const int8_t *__restrict__ Xq, const int8_t *__restrict__ Wq, const float *__restrict__ sX,
-    const float *__restrict__ sW, const float *__restrict__ bp, int M, int N, int K,
-    uint16_t *__restrict__ Y, int32_t *__restrict__ acc_out) {
+    const int32_t *__restrict__ zW, const float *__restrict__ sW, const float *__restrict__ bp,
+    int M, int N, int K, uint16_t *__restrict__ Y, int32_t *__restrict__ acc_out) {
   __shared__ __attribute__((aligned(1024)))
   int8_t smem[S * DecodeCfg<MB, NR, NK, RBW, BKD, S>::kStage];
-  decode_body<MB, NR, NK, RBW, BKD, S, PT>(smem, Xq, Wq, sX, sW, bp, M, N, K, Y, acc_out);
+  decode_body<MB, NR, NK, RBW, BKD, S, EPI>(smem, Xq, Wq, sX, zW, sW, bp, M, N, K, Y, acc_out);
 }
 
-// sX == nullptr: per-channel epilogue; else per-token scales sX [M].
+// Epilogue by argument: sX != nullptr per-token scales sX [M]; zW != nullptr
+// asymmetric weight zero points zW [N]; neither: per-channel.
 template <int MB, int NR, int NK, int RBW, int BKD, int S>
-hipError_t launch_decode(const int8_t *Xq, const int8_t *Wq, const float *sX, const float *sW,
-                         const float *bp, int64_t M, int64_t N, int64_t K, uint16_t *Y,
-                         int32_t *acc_out, hipStream_t st) {
+hipError_t launch_decode(const int8_t *Xq, const int8_t *Wq, const float *sX, const int32_t *zW,
+                         const float *sW, const float *bp, int64_t M, int64_t N, int64_t K,
+                         uint16_t *Y, int32_t *acc_out, hipStream_t st) {
   constexpr int rows = 16 * RBW * NR;
   const unsigned grid = (unsigned)((N + rows - 1) / rows);
+  const dim3 block(64 * NR * NK);
   if (sX)
-    qgemm_decode_kernel<MB, NR, NK, RBW, BKD, S, true><<<grid, 64 * NR * NK, 0, st>>>(
-        Xq, Wq, sX, sW, bp, (int)M, (int)N, (int)K, Y, acc_out);
+    qgemm_decode_kernel<MB, NR, NK, RBW, BKD, S, kEpiToken><<<grid, block, 0, st>>>(
+        Xq, Wq, sX, zW, sW, bp, (int)M, (int)N, (int)K, Y, acc_out);
+  else if (zW)
+    qgemm_decode_kernel<MB, NR, NK, RBW, BKD, S, kEpiAsym><<<grid, block, 0, st>>>(
+        Xq, Wq, sX, zW, sW, bp, (int)M, (int)N, (int)K, Y, acc_out);
   else
-    qgemm_decode_kernel<MB, NR, NK, RBW, BKD, S, false><<<grid, 64 * NR * NK, 0, st>>>(
-        Xq, Wq, sX, sW, bp, (int)M, (int)N, (int)K, Y, acc_out);
+    qgemm_decode_kernel<MB, NR, NK, RBW, BKD, S, kEpiChannel><<<grid, block, 0, st>>>(
+        Xq, Wq, sX, zW, sW, bp, (int)M, (int)N, (int)K, Y, acc_out);
   return hipGetLastError();
 }
 
@@ -216,8 +250,9 @@ hipError_t launch_decode(const int8_t *Xq, const int8_t *Wq, const float *sX, co
 using namespace detail;
 
 hipError_t launch_qgemm_decode(const int8_t *Xq, const int8_t *Wq, const float *sX,
-                               const float *sW, const float *bprime, int64_t M, int64_t N,
-                               int64_t K, uint16_t *Y, int32_t *acc_out, hipStream_t st) {
+                               const int32_t *zW, const float *sW, const float *bprime,
+                               int64_t M, int64_t N, int64_t K, uint16_t *Y, int32_t *acc_out,
+                               hipStream_t st) {
   // Template arguments
   // <token blocks, row groups, K groups, row blocks per wave, BKD, stages>.
   // Up to 16 tokens the workgroup is one 16-row block split over 4 K groups
@@ -227,17 +262,17 @@ hipError_t launch_qgemm_decode(const int8_t *Xq, const int8_t *Wq, const float *
   // pass over the 256 CUs (taller tiles re-read the token tile less, shorter
   // ones use more CUs); past 128 rows x 256 CUs, 64-row tiles keep the last
   // pass's tail short.
-  if (M <= 16) return launch_decode<1, 1, 4, 1, 256, 4>(Xq, Wq, sX, sW, bprime, M, N, K, Y, acc_out, st);
+  if (M <= 16) return launch_decode<1, 1, 4, 1, 256, 4>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, st);
   constexpr int64_t kCUs = 256;
   const int rows = N <= 32 * kCUs ? 32 : N <= 64 * kCUs ? 64 : N <= 128 * kCUs ? 128 : 64;
   if (M <= 32) {
-    if (rows == 32) return launch_decode<2, 2, 4, 1, 256, 4>(Xq, Wq, sX, sW, bprime, M, N, K, Y, acc_out, st);
-    if (rows == 64) return launch_decode<2, 4, 2, 1, 256, 3>(Xq, Wq, sX, sW, bprime, M, N, K, Y, acc_out, st);
-    return launch_decode<2, 4, 2, 2, 256, 3>(Xq, Wq, sX, sW, bprime, M, N, K, Y, acc_out, st);
+    if (rows == 32) return launch_decode<2, 2, 4, 1, 256, 4>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, st);
+    if (rows == 64) return launch_decode<2, 4, 2, 1, 256, 3>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, st);
+    return launch_decode<2, 4, 2, 2, 256, 3>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, st);
   }
-  if (rows == 32) return launch_decode<4, 2, 4, 1, 256, 4>(Xq, Wq, sX, sW, bprime, M, N, K, Y, acc_out, st);
-  if (rows == 64) return launch_decode<4, 4, 2, 1, 256, 3>(Xq, Wq, sX, sW, bprime, M, N, K, Y, acc_out, st);
-  return launch_decode<4, 4, 2, 2, 256, 3>(Xq, Wq, sX, sW, bprime, M, N, K, Y, acc_out, st);
+  if (rows == 32) return launch_decode<4, 2, 4, 1, 256, 4>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, st);
+  if (rows == 64) return launch_decode<4, 4, 2, 1, 256, 3>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, st);
+  return launch_decode<4, 4, 2, 2, 256, 3>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, st);
 }
 
 }  // namespace ot

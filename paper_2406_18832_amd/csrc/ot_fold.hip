@@ -85,6 +85,72 @@ __global__ __launch_bounds__(kThreads) void fold_kernel(const uint16_t *__restri
   }
 }
 
+// Asymmetric weights (the "Int8" setting): per output channel n of W_s,
+//   lo, hi = min(min_k W_s, 0), max(max_k W_s, 0);  sW = fp32((hi - lo) / L)
+//   zW = clip(rne(-lo / sW), 0, L);  c = clip(rne(W_s / sW) + zW, 0, L)
+// with L = 2^bits - 1 (Eq. (a) with a zero point).  Codes and zero point
+// are stored shifted by 2^(bits-1) (signed int8 for the matrix cores).
+__global__ __launch_bounds__(kThreads) void fold_asym_kernel(
+    const uint16_t *__restrict__ W, const uint16_t *__restrict__ b, int64_t K, int w_bits,
+    const float *__restrict__ z, const float *__restrict__ s, int8_t *__restrict__ Wq,
+    float *__restrict__ sW, int32_t *__restrict__ zW, float *__restrict__ bprime) {
+  __shared__ double red_min[kThreads];
+  __shared__ double red_max[kThreads];
+  __shared__ double red_sum[kThreads];
+  __shared__ int red_bad[kThreads];
+  __shared__ double row_scale, row_zero;
+
+  const int64_t n = blockIdx.x;
+  const uint16_t *w = W + n * K;
+  const int t = threadIdx.x;
+  const double L = (double)((1 << w_bits) - 1);
+  const int half = 1 << (w_bits - 1);
+
+  double lo = 0.0, hi = 0.0, acc = 0.0;  // the range always holds 0
+  int bad = 0;
+  for (int64_t k = t; k < K; k += kThreads) {
+    const double wk = (double)half_bits_to_float(w[k]);
+    bad |= !isfinite(wk);
+    const double ws = (double)s[k] * wk;  // Eq. (e), exact
+    lo = fmin(lo, ws);
+    hi = fmax(hi, ws);
+    acc += (double)z[k] * wk;  // exact product, fp64 sum
+  }
+  red_min[t] = lo;
+  red_max[t] = hi;
+  red_sum[t] = acc;
+  red_bad[t] = bad;
+  __syncthreads();
+  for (int off = kThreads / 2; off > 0; off >>= 1) {
+    if (t < off) {
+      red_min[t] = fmin(red_min[t], red_min[t + off]);
+      red_max[t] = fmax(red_max[t], red_max[t + off]);
+      red_sum[t] = red_sum[t] + red_sum[t + off];
+      red_bad[t] |= red_bad[t + off];
+    }
+    __syncthreads();
+  }
+  if (t == 0) {
+    float sw = (float)((red_max[0] - red_min[0]) / L);
+    if (sw == 0.0f) sw = 1.0f;
+    const double zp = fmin(fmax(rint(-red_min[0] / (double)sw), 0.0), L);
+    const double bn = b ? (double)half_bits_to_float(b[n]) : 0.0;
+    sW[n] = red_bad[0] ? __builtin_nanf("") : sw;  // the host checks sW
+    zW[n] = (int32_t)zp - half;
+    bprime[n] = (float)(red_sum[0] + bn);
+    row_scale = (double)sw;
+    row_zero = zp;
+  }
+  __syncthreads();
+  const double sc = row_scale, zp = row_zero;
+  int8_t *q = Wq + n * K;
+  for (int64_t k = t; k < K; k += kThreads) {
+    const double ws = (double)s[k] * (double)half_bits_to_float(w[k]);
+    const double c = fmin(fmax(rint(ws / sc) + zp, 0.0), L);
+    q[k] = (int8_t)((int)c - half);
+  }
+}
+
 }  // namespace detail
 
 using namespace detail;
@@ -103,6 +169,13 @@ hipError_t launch_fold_per_token(const uint16_t *W, const uint16_t *b, const flo
                                  float *bprime, hipStream_t st) {
   fold_kernel<<<(unsigned)N, kThreads, 0, st>>>(W, b, zres, K, qw, nullptr, nullptr, Wq, sW,
                                                 bprime);
+  return hipGetLastError();
+}
+
+hipError_t launch_fold_asym(const uint16_t *W, const uint16_t *b, int64_t N, int64_t K,
+                            int w_bits, const float *z, const float *s, int8_t *Wq, float *sW,
+                            int32_t *zW, float *bprime, hipStream_t st) {
+  fold_asym_kernel<<<(unsigned)N, kThreads, 0, st>>>(W, b, K, w_bits, z, s, Wq, sW, zW, bprime);
   return hipGetLastError();
 }
 

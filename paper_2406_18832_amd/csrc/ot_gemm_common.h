@@ -47,42 +47,77 @@ __device__ inline uint16_t dequant_pt(int a, float sx, float sw, float bp) {
   return float_to_half_bits(y);
 }
 
-// Epilogue flavours: PT = false is the per-channel path (one scale per
-// output channel), PT = true the per-token path (token scale sx as well).
-template <bool PT>
+// Epilogue flavours
+//   kEpiChannel  per-channel path, Eq. (g): scale per output channel
+//   kEpiToken    per-token path, Eq. (c): token scale sx as well
+//   kEpiAsym     asymmetric weights, Eq. (a): the integer sum becomes
+//                acc - zW[n] * rowsum(Xq[m]) before the per-channel scale
+constexpr int kEpiChannel = 0, kEpiToken = 1, kEpiAsym = 2;
+
+template <int EPI>
 __device__ inline uint16_t dequant_x(int a, float sx, float sw, float bp) {
-  if constexpr (PT) return dequant_pt(a, sx, sw, bp);
+  if constexpr (EPI == kEpiToken) return dequant_pt(a, sx, sw, bp);
   else return dequant(a, sw, bp);
 }
 
-// Writes four consecutive channels n..n+3 of token m (token scale sx, used
-// when PT).
-template <bool PT>
+// Four consecutive weight zero points n..n+3 (zeros past N; unused unless
+// EPI == kEpiAsym).
+template <int EPI>
+__device__ inline int4 load_zw4(const int32_t *__restrict__ zW, int64_t n, int64_t N) {
+  if constexpr (EPI != kEpiAsym) {
+    return make_int4(0, 0, 0, 0);
+  } else {
+    if (n + 3 < N && (N & 3) == 0) return *reinterpret_cast<const int4 *>(zW + n);
+    return make_int4(n < N ? zW[n] : 0, n + 1 < N ? zW[n + 1] : 0, n + 2 < N ? zW[n + 2] : 0,
+                     n + 3 < N ? zW[n + 3] : 0);
+  }
+}
+
+// Writes four consecutive channels n..n+3 of token m.  sx is the token's
+// scale (kEpiToken), rs its code sum (kEpiAsym); acc_out receives the
+// integer sum the epilogue scales.
+template <int EPI>
 __device__ inline void store4(uint16_t *__restrict__ Y, int32_t *__restrict__ acc_out,
                               const float *__restrict__ sW, const float *__restrict__ bp,
-                              float sx, int64_t m, int64_t n, int64_t M, int64_t N, int a0,
-                              int a1, int a2, int a3) {
+                              const int32_t *__restrict__ zW, float sx, int rs, int64_t m,
+                              int64_t n, int64_t M, int64_t N, int a0, int a1, int a2, int a3) {
   if (m >= M) return;
+  if constexpr (EPI == kEpiAsym) {
+    const int4 z4 = load_zw4<EPI>(zW, n, N);
+    a0 -= z4.x * rs;
+    a1 -= z4.y * rs;
+    a2 -= z4.z * rs;
+    a3 -= z4.w * rs;
+  }
   const int64_t base = m * N + n;
   if (n + 3 < N && (N & 3) == 0) {
     const float4 s4 = *reinterpret_cast<const float4 *>(sW + n);
     const float4 b4 = *reinterpret_cast<const float4 *>(bp + n);
     uint2 o;
-    o.x = (uint32_t)dequant_x<PT>(a0, sx, s4.x, b4.x) |
-          ((uint32_t)dequant_x<PT>(a1, sx, s4.y, b4.y) << 16);
-    o.y = (uint32_t)dequant_x<PT>(a2, sx, s4.z, b4.z) |
-          ((uint32_t)dequant_x<PT>(a3, sx, s4.w, b4.w) << 16);
+    o.x = (uint32_t)dequant_x<EPI>(a0, sx, s4.x, b4.x) |
+          ((uint32_t)dequant_x<EPI>(a1, sx, s4.y, b4.y) << 16);
+    o.y = (uint32_t)dequant_x<EPI>(a2, sx, s4.z, b4.z) |
+          ((uint32_t)dequant_x<EPI>(a3, sx, s4.w, b4.w) << 16);
     *reinterpret_cast<uint2 *>(Y + base) = o;
     if (acc_out) *reinterpret_cast<int4 *>(acc_out + base) = make_int4(a0, a1, a2, a3);
   } else {
     const int a[4] = {a0, a1, a2, a3};
     for (int i = 0; i < 4; ++i) {
       if (n + i < N) {
-        Y[base + i] = dequant_x<PT>(a[i], sx, sW[n + i], bp[n + i]);
+        Y[base + i] = dequant_x<EPI>(a[i], sx, sW[n + i], bp[n + i]);
         if (acc_out) acc_out[base + i] = a[i];
       }
     }
   }
+}
+
+// Sum of the 16 signed bytes of a fragment (one dot-product instruction per
+// 4 bytes against all-ones).
+__device__ inline int byte_sum16(v4i f, int acc) {
+  acc = __builtin_amdgcn_sdot4(f[0], 0x01010101, acc, false);
+  acc = __builtin_amdgcn_sdot4(f[1], 0x01010101, acc, false);
+  acc = __builtin_amdgcn_sdot4(f[2], 0x01010101, acc, false);
+  return __builtin_amdgcn_sdot4(f[3], 0x01010101, acc, false);
 }
 
 typedef __attribute__((address_space(3))) void lds_void;

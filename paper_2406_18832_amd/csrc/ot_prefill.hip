@@ -79,12 +79,12 @@ __device__ __forceinline__ void sched_interleave() {
 
 // The kernel body lives in a device function: hipcc drops the host stub of a
 // kernel template whose body holds lambdas.
-template <int BN, int BM, int BK, int WN, int WM, int S, bool PT>
+template <int BN, int BM, int BK, int WN, int WM, int S, int EPI>
 __device__ __forceinline__ void prefill_body(
     int8_t *smem, const int8_t *__restrict__ Xq, const int8_t *__restrict__ Wq,
-    const float *__restrict__ sX, const float *__restrict__ sW, const float *__restrict__ bp,
-    int M, int N, int K, uint16_t *__restrict__ Y, int32_t *__restrict__ acc_out, int tiles_m,
-    int tiles_n, int group_m) {
+    const float *__restrict__ sX, const int32_t *__restrict__ zW, const float *__restrict__ sW,
+    const float *__restrict__ bp, int M, int N, int K, uint16_t *__restrict__ Y,
+    int32_t *__restrict__ acc_out, int tiles_m, int tiles_n, int group_m) {
   using C = PrefillCfg<BN, BM, BK, WN, WM, S>;
 
   // ---- tile schedule ------------------------------------------------------
@@ -176,12 +176,21 @@ __device__ __forceinline__ void prefill_body(
   for (int f = 0; f < C::kFN; ++f)
 #pragma unroll
     for (int g = 0; g < C::kFM; ++g) acc[f][g] = v16i{};
+  // asymmetric weights: each lane also sums the token bytes it feeds to the
+  // matrix cores (its token fr, half fh of every K step)
+  int rs[C::kFM];
+#pragma unroll
+  for (int g = 0; g < C::kFM; ++g) rs[g] = 0;
   auto mfmas = [&](int buf) {
 #pragma unroll
     for (int f = 0; f < C::kFN; ++f)
 #pragma unroll
       for (int g = 0; g < C::kFM; ++g)
         acc[f][g] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fa[buf][f], fb[buf][g], acc[f][g], 0, 0, 0);
+    if constexpr (EPI == kEpiAsym) {
+#pragma unroll
+      for (int g = 0; g < C::kFM; ++g) rs[g] = byte_sum16(fb[buf][g], rs[g]);
+    }
   };
 
   // ---- main loop ----------------------------------------------------------------
@@ -225,12 +234,14 @@ __device__ __forceinline__ void prefill_body(
   // and rows 8*(r/4) + 4*(l/32) + (r mod 4) for register r.  Columns are
   // tokens here and rows are channels, so registers 4j..4j+3 are four
   // consecutive channels of one token.
-  // token scales of this lane's tokens (per-token path only)
+  // token scales of this lane's tokens (per-token path), and the full code
+  // sums of its tokens (asymmetric weights: the two K halves meet)
   float sx[C::kFM];
 #pragma unroll
   for (int g = 0; g < C::kFM; ++g) {
     const int m = m0 + wm * C::kTM + g * 32 + fr;
-    sx[g] = (PT && m < M) ? sX[m] : 0.f;
+    sx[g] = (EPI == kEpiToken && m < M) ? sX[m] : 0.f;
+    if constexpr (EPI == kEpiAsym) rs[g] += __shfl_xor(rs[g], 32);
   }
   if (acc_out != nullptr) {  // test path: also stores the raw accumulators
 #pragma unroll
@@ -241,8 +252,8 @@ __device__ __forceinline__ void prefill_body(
 #pragma unroll
         for (int g = 0; g < C::kFM; ++g) {
           const int64_t m = m0 + wm * C::kTM + g * 32 + fr;
-          store4<PT>(Y, acc_out, sW, bp, sx[g], m, n, M, N, acc[f][g][4 * j],
-                     acc[f][g][4 * j + 1], acc[f][g][4 * j + 2], acc[f][g][4 * j + 3]);
+          store4<EPI>(Y, acc_out, sW, bp, zW, sx[g], rs[g], m, n, M, N, acc[f][g][4 * j],
+                      acc[f][g][4 * j + 1], acc[f][g][4 * j + 2], acc[f][g][4 * j + 3]);
         }
       }
     return;
@@ -278,14 +289,19 @@ __device__ __forceinline__ void prefill_body(
         if (n + 2 < N) { s4.z = sW[n + 2]; b4.z = bp[n + 2]; }
         if (n + 3 < N) { s4.w = sW[n + 3]; b4.w = bp[n + 3]; }
       }
+      const int4 z4 = load_zw4<EPI>(zW, n, N);
 #pragma unroll
       for (int g = 0; g < C::kFM; ++g) {
         const int ml = g * 32 + fr;
         uint2 h;
-        h.x = (uint32_t)dequant_x<PT>(acc[f][g][4 * j + 0], sx[g], s4.x, b4.x) |
-              ((uint32_t)dequant_x<PT>(acc[f][g][4 * j + 1], sx[g], s4.y, b4.y) << 16);
-        h.y = (uint32_t)dequant_x<PT>(acc[f][g][4 * j + 2], sx[g], s4.z, b4.z) |
-              ((uint32_t)dequant_x<PT>(acc[f][g][4 * j + 3], sx[g], s4.w, b4.w) << 16);
+        const int a0 = acc[f][g][4 * j + 0] - z4.x * rs[g];
+        const int a1 = acc[f][g][4 * j + 1] - z4.y * rs[g];
+        const int a2 = acc[f][g][4 * j + 2] - z4.z * rs[g];
+        const int a3 = acc[f][g][4 * j + 3] - z4.w * rs[g];
+        h.x = (uint32_t)dequant_x<EPI>(a0, sx[g], s4.x, b4.x) |
+              ((uint32_t)dequant_x<EPI>(a1, sx[g], s4.y, b4.y) << 16);
+        h.y = (uint32_t)dequant_x<EPI>(a2, sx[g], s4.z, b4.z) |
+              ((uint32_t)dequant_x<EPI>(a3, sx[g], s4.w, b4.w) << 16);
         const int unit = (nl >> 2) ^ (ml & (kUnits - 1));
         *reinterpret_cast<uint2 *>(tile + ml * C::kTN + unit * 4) = h;
       }
@@ -324,31 +340,36 @@ __device__ __forceinline__ void prefill_body(
 
 }
 
-template <int BN, int BM, int BK, int WN, int WM, int S, int OCC, bool PT>
+template <int BN, int BM, int BK, int WN, int WM, int S, int OCC, int EPI>
 __global__ __launch_bounds__(64 * WN * WM, OCC) void qgemm_prefill_kernel(
     const int8_t *__restrict__ Xq, const int8_t *__restrict__ Wq, const float *__restrict__ sX,
-    const float *__restrict__ sW, const float *__restrict__ bp, int M, int N, int K,
-    uint16_t *__restrict__ Y, int32_t *__restrict__ acc_out, int tiles_m, int tiles_n,
-    int group_m) {
+    const int32_t *__restrict__ zW, const float *__restrict__ sW, const float *__restrict__ bp,
+    int M, int N, int K, uint16_t *__restrict__ Y, int32_t *__restrict__ acc_out, int tiles_m,
+    int tiles_n, int group_m) {
   __shared__ __attribute__((aligned(1024)))
   int8_t smem[S * PrefillCfg<BN, BM, BK, WN, WM, S>::kStage];
-  prefill_body<BN, BM, BK, WN, WM, S, PT>(smem, Xq, Wq, sX, sW, bp, M, N, K, Y, acc_out,
-                                          tiles_m, tiles_n, group_m);
+  prefill_body<BN, BM, BK, WN, WM, S, EPI>(smem, Xq, Wq, sX, zW, sW, bp, M, N, K, Y, acc_out,
+                                           tiles_m, tiles_n, group_m);
 }
 
-// sX == nullptr: per-channel epilogue; else per-token scales sX [M].
+// Epilogue by argument: sX != nullptr per-token scales sX [M]; zW != nullptr
+// asymmetric weight zero points zW [N]; neither: per-channel.
 template <int BN, int BM, int BK, int WN, int WM, int S, int OCC = 1>
-hipError_t launch_prefill(const int8_t *Xq, const int8_t *Wq, const float *sX, const float *sW,
-                          const float *bp, int64_t M, int64_t N, int64_t K, uint16_t *Y,
-                          int32_t *acc_out, hipStream_t st, int group_m = 8) {
+hipError_t launch_prefill(const int8_t *Xq, const int8_t *Wq, const float *sX, const int32_t *zW,
+                          const float *sW, const float *bp, int64_t M, int64_t N, int64_t K,
+                          uint16_t *Y, int32_t *acc_out, hipStream_t st, int group_m = 8) {
   const int tiles_m = (int)((M + BM - 1) / BM), tiles_n = (int)((N + BN - 1) / BN);
   const unsigned grid = (unsigned)(tiles_m * tiles_n);
+  const dim3 block(64 * WN * WM);
   if (sX)
-    qgemm_prefill_kernel<BN, BM, BK, WN, WM, S, OCC, true><<<grid, 64 * WN * WM, 0, st>>>(
-        Xq, Wq, sX, sW, bp, (int)M, (int)N, (int)K, Y, acc_out, tiles_m, tiles_n, group_m);
+    qgemm_prefill_kernel<BN, BM, BK, WN, WM, S, OCC, kEpiToken><<<grid, block, 0, st>>>(
+        Xq, Wq, sX, zW, sW, bp, (int)M, (int)N, (int)K, Y, acc_out, tiles_m, tiles_n, group_m);
+  else if (zW)
+    qgemm_prefill_kernel<BN, BM, BK, WN, WM, S, OCC, kEpiAsym><<<grid, block, 0, st>>>(
+        Xq, Wq, sX, zW, sW, bp, (int)M, (int)N, (int)K, Y, acc_out, tiles_m, tiles_n, group_m);
   else
-    qgemm_prefill_kernel<BN, BM, BK, WN, WM, S, OCC, false><<<grid, 64 * WN * WM, 0, st>>>(
-        Xq, Wq, sX, sW, bp, (int)M, (int)N, (int)K, Y, acc_out, tiles_m, tiles_n, group_m);
+    qgemm_prefill_kernel<BN, BM, BK, WN, WM, S, OCC, kEpiChannel><<<grid, block, 0, st>>>(
+        Xq, Wq, sX, zW, sW, bp, (int)M, (int)N, (int)K, Y, acc_out, tiles_m, tiles_n, group_m);
   return hipGetLastError();
 }
 
@@ -359,9 +380,11 @@ using namespace detail;
 // One tile shape for every prefill layer: 256x256 output tiles, BK = 128,
 // 8 waves as 4 (weight rows) x 2 (tokens), a 2-stage ring (128 KiB of LDS).
 hipError_t launch_qgemm_prefill(const int8_t *Xq, const int8_t *Wq, const float *sX,
-                                const float *sW, const float *bprime, int64_t M, int64_t N,
-                                int64_t K, uint16_t *Y, int32_t *acc_out, hipStream_t st) {
-  return launch_prefill<256, 256, 128, 4, 2, 2>(Xq, Wq, sX, sW, bprime, M, N, K, Y, acc_out, st);
+                                const int32_t *zW, const float *sW, const float *bprime,
+                                int64_t M, int64_t N, int64_t K, uint16_t *Y, int32_t *acc_out,
+                                hipStream_t st) {
+  return launch_prefill<256, 256, 128, 4, 2, 2>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out,
+                                                st);
 }
 
 }  // namespace ot

@@ -7,13 +7,14 @@ namespace ot {
 
 // At most 64 tokens (decode) the GEMM streams the weights once and is bound
 // by HBM bandwidth; beyond that (prefill) it is a tiled int8 MFMA GEMM.
-// sX == nullptr selects the per-channel epilogue of Eq. (g), else the
-// per-token epilogue of Eq. (c) with token scales sX [M].
-hipError_t launch_qgemm(const int8_t *Xq, const int8_t *Wq, const float *sX, const float *sW,
-                        const float *bprime, int64_t M, int64_t N, int64_t K, uint16_t *Y,
-                        int32_t *acc_out, hipStream_t st) {
-  if (M <= 64) return launch_qgemm_decode(Xq, Wq, sX, sW, bprime, M, N, K, Y, acc_out, st);
-  return launch_qgemm_prefill(Xq, Wq, sX, sW, bprime, M, N, K, Y, acc_out, st);
+// Epilogue: sX != nullptr the per-token scales of Eq. (c); zW != nullptr the
+// asymmetric weight zero points of Eq. (a); neither, the per-channel
+// epilogue of Eq. (g).
+hipError_t launch_qgemm(const int8_t *Xq, const int8_t *Wq, const float *sX, const int32_t *zW,
+                        const float *sW, const float *bprime, int64_t M, int64_t N, int64_t K,
+                        uint16_t *Y, int32_t *acc_out, hipStream_t st) {
+  if (M <= 64) return launch_qgemm_decode(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, st);
+  return launch_qgemm_prefill(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, st);
 }
 
 }  // namespace ot

@@ -62,6 +62,11 @@ def lib() -> ctypes.CDLL:
                                            vp, vp]
         L.ot_scales_from_minmax.restype = c_int
         L.ot_scales_from_minmax.argtypes = [vp, i64, c_int, c_int, vp, vp, vp, vp]
+        L.ot_fold_weights_asym.restype = c_int
+        L.ot_fold_weights_asym.argtypes = [vp, vp, i64, i64, c_int, vp, vp, vp, vp, vp, vp, vp]
+        L.ot_qlinear_asym.restype = c_int
+        L.ot_qlinear_asym.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, c_int, c_int, vp, vp, vp,
+                                      vp]
         L.ot_qlinear.restype = c_int
         L.ot_qlinear.argtypes = [vp, vp, vp, vp, i64, i64, i64, c_int, c_int, vp, vp, vp, vp]
         L.ot_qlinear_workspace_size.restype = ctypes.c_size_t
@@ -247,6 +252,39 @@ def ot_qlinear_per_token(Xq, Wq, sX, sW, bprime, a_bits, w_bits, Y, acc_out=None
     _check(rc, "ot_qlinear_per_token")
 
 
+def ot_fold_weights_asym(W, b, w_bits, z, s, Wq, sW, zW, bprime, stream=None):
+    """Asymmetric ("Int8") weights: W [N, K] fp16, b [N] fp16 or None ->
+    shifted codes Wq [N, K] int8, sW [N] fp32, shifted zero points zW [N]
+    int32, bprime [N] fp32.  Synchronous."""
+    N, K = W.shape
+    rc = lib().ot_fold_weights_asym(_dev(W, torch.float16, "W"), _dev(b, torch.float16, "b", (N,)),
+                                    N, K, int(w_bits), _dev(z, torch.float32, "z", (K,)),
+                                    _dev(s, torch.float32, "s", (K,)),
+                                    _dev(Wq, torch.int8, "Wq", (N, K)),
+                                    _dev(sW, torch.float32, "sW", (N,)),
+                                    _dev(zW, torch.int32, "zW", (N,)),
+                                    _dev(bprime, torch.float32, "bprime", (N,)), _stream(stream))
+    _check(rc, "ot_fold_weights_asym")
+
+
+def ot_qlinear_asym(Xq, Wq, sW, zW, bprime, a_bits, w_bits, Y, acc_out=None, workspace=None,
+                    stream=None):
+    """Quantized linear with asymmetric weights: acc = Xq (Wq - zW)^T, then
+    the per-channel epilogue.  Asynchronous."""
+    M, K = Xq.shape
+    N = Wq.shape[0]
+    if Wq.shape[1] != K:
+        raise ValueError("Xq and Wq disagree on K")
+    rc = lib().ot_qlinear_asym(_dev(Xq, torch.int8, "Xq"), _dev(Wq, torch.int8, "Wq"),
+                               _dev(sW, torch.float32, "sW", (N,)),
+                               _dev(zW, torch.int32, "zW", (N,)),
+                               _dev(bprime, torch.float32, "bprime", (N,)), M, N, K, int(a_bits),
+                               int(w_bits), _dev(Y, torch.float16, "Y", (M, N)),
+                               _dev(acc_out, torch.int32, "acc_out", (M, N)),
+                               None if workspace is None else workspace.data_ptr(), _stream(stream))
+    _check(rc, "ot_qlinear_asym")
+
+
 def calibrate(batches, a_bits, device="cuda"):
     """Runs ot_calibrate over an iterable of fp16 [rows, K] batches (host
     numpy or device tensors).  Returns (minmax, z, s, inv_s) on the GPU."""
@@ -319,4 +357,22 @@ def qlinear_per_token(Xq, Wq, sX, sW, bprime, a_bits, w_bits, want_acc=False):
     Y = torch.empty((M, N), dtype=torch.float16, device=Xq.device)
     acc = torch.empty((M, N), dtype=torch.int32, device=Xq.device) if want_acc else None
     ot_qlinear_per_token(Xq, Wq, sX, sW, bprime, a_bits, w_bits, Y, acc)
+    return (Y, acc) if want_acc else Y
+
+
+def fold_weights_asym(W, b, w_bits, z, s):
+    N, K = W.shape
+    Wq = torch.empty((N, K), dtype=torch.int8, device=W.device)
+    sW = torch.empty(N, dtype=torch.float32, device=W.device)
+    zW = torch.empty(N, dtype=torch.int32, device=W.device)
+    bprime = torch.empty(N, dtype=torch.float32, device=W.device)
+    ot_fold_weights_asym(W, b, w_bits, z, s, Wq, sW, zW, bprime)
+    return Wq, sW, zW, bprime
+
+
+def qlinear_asym(Xq, Wq, sW, zW, bprime, a_bits, w_bits, want_acc=False):
+    M, N = Xq.shape[0], Wq.shape[0]
+    Y = torch.empty((M, N), dtype=torch.float16, device=Xq.device)
+    acc = torch.empty((M, N), dtype=torch.int32, device=Xq.device) if want_acc else None
+    ot_qlinear_asym(Xq, Wq, sW, zW, bprime, a_bits, w_bits, Y, acc)
     return (Y, acc) if want_acc else Y

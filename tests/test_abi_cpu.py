@@ -110,6 +110,20 @@ def test_per_token_argument_checks():
     assert g(16, 16, NULL, 16, 16, 4, 8, 32, 8, 8, 16, NULL, NULL, NULL) == ot.OT_EINVAL
 
 
+def test_asym_argument_checks():
+    L = ot.lib()
+    f = L.ot_fold_weights_asym
+    assert f(NULL, NULL, 8, 32, 8, NULL, NULL, NULL, NULL, NULL, NULL, NULL) == ot.OT_EINVAL
+    assert f(16, NULL, 0, 32, 8, 16, 16, 16, 16, 16, 16, NULL) == ot.OT_ESHAPE
+    assert f(16, NULL, 8, 32, 1, 16, 16, 16, 16, 16, 16, NULL) == ot.OT_EINVAL
+    g = L.ot_qlinear_asym
+    assert g(NULL, NULL, NULL, NULL, NULL, 4, 8, 24, 8, 8, NULL, NULL, NULL, NULL) == ot.OT_ESHAPE
+    # K qa 2^w_bits >= 2^31: 66064 * 127 * 256 > 2^31, 66048 * 127 * 256 < 2^31
+    assert g(NULL, NULL, NULL, NULL, NULL, 4, 8, 66064, 8, 8, NULL, NULL, NULL, NULL) == ot.OT_ERANGE
+    assert g(NULL, NULL, NULL, NULL, NULL, 0, 8, 66048, 8, 8, NULL, NULL, NULL, NULL) == ot.OT_OK
+    assert g(16, 16, 16, NULL, 16, 4, 8, 32, 8, 8, 16, NULL, NULL, NULL) == ot.OT_EINVAL
+
+
 def test_calibrate_and_fold_argument_checks():
     L = ot.lib()
     assert L.ot_calibrate(NULL, 4, 32, 8, 1, NULL, NULL, NULL, NULL, NULL) == ot.OT_EINVAL
