@@ -13,7 +13,8 @@ Printed: one JSON line.  `value` is int8 TOPS over the whole step (GEMM ops
 measured by HIP events around each launch inside the timed region; the
 decode regime (OPT-30B shapes, M in {1, 8, 32, 64}) is reported under
 `decode` in GB/s against HBM; `mixed_block` times the paper's own split
-(per-channel qkv/fc1, per-token out/fc2); `ln_quantize` times the LayerNorm fused with
+(per-channel qkv/fc1, per-token out/fc2); `asym_weights` the main step with
+asymmetric ("Int8") weights; `ln_quantize` times the LayerNorm fused with
 symmetrization and quantization (qkv and fc1 inputs) against torch's
 LayerNorm plus ot_quantize_act; `fp16_baseline` times torch's fp16 linear on
 the same shapes; `cpu_baseline` times the CPU oracle on a bounded sample.
@@ -50,6 +51,8 @@ def parse():
     p.add_argument("--no-fp16", action="store_true", help="skip the fp16 torch baseline")
     p.add_argument("--no-cpu", action="store_true", help="skip the CPU-oracle baseline")
     p.add_argument("--no-ln", action="store_true", help="skip the fused LayerNorm report")
+    p.add_argument("--no-asym", action="store_true",
+                   help="skip the asymmetric-weight step report")
     p.add_argument("--no-mixed", action="store_true",
                    help="skip the per-channel + per-token block report")
     p.add_argument("--iters", type=int, default=50, help="iterations for the side measurements")
@@ -201,6 +204,27 @@ def mixed_block_report(torch, ot, wl, layers, iters):
     return dict(ms_per_step=med, p10_ms=p10, p90_ms=p90, tops=ops / (med * 1e-3) / 1e12,
                 per_token_quantize_fc2_us=qmed * 1e3,
                 per_token_quantize_fc2_GBps=qbytes / (qmed * 1e-3) / 1e9)
+
+
+def asym_report(torch, ot, wl, layers, iters):
+    """Asymmetric ("Int8") weights on the main step: the same quantized
+    activations against zero-point weight codes (folded untimed from the same
+    fp16 weights); the GEMM also forms each token's code sum and subtracts
+    zW * sum in the epilogue."""
+    M = wl.M
+    plan = []
+    for L in layers:
+        Wq, sW, zW, bp = ot.fold_weights_asym(L["W16"], L["b16"], wl.w_bits, L["z"], L["s"])
+        plan.append((L, Wq, sW, zW, bp))
+
+    def step():
+        for L, Wq, sW, zW, bp in plan:
+            ot.ot_quantize_act(L["X"], wl.a_bits, L["z"], L["inv_s"], L["Xq"])
+            ot.ot_qlinear_asym(L["Xq"], Wq, sW, zW, bp, wl.a_bits, wl.w_bits, L["Y"])
+    med, p10, p90 = median_ms(torch, step, iters)
+    ops = sum(2.0 * M * L["N"] * L["K"] for L in layers)
+    log(f"asymmetric-weight step: {med:.3f} ms ({ops / (med * 1e-3) / 1e12:.0f} TOPS)")
+    return dict(ms_per_step=med, p10_ms=p10, p90_ms=p90, tops=ops / (med * 1e-3) / 1e12)
 
 
 def decode_report(torch, ot, synth, wl, pool, iters, with_fp16):
@@ -364,7 +388,8 @@ def traffic_record(d, workload):
                               "bytes": (f * factors["FETCH_SIZE"] + w * factors["WRITE_SIZE"]) * 1024}
         alg[L.name] = wl.M * L.K + L.N * L.K + 2 * wl.M * L.N + 8 * L.N
     cmd = "cd /tmp && timeout -s KILL 120 rocprofv3 --pmc {c} --output-format csv -d <out>/{sub} -o p -- python -u <repo>/bench.py {args}"
-    bench_args = "--steps 2 --warmup 1 --no-cpu --no-fp16 --no-decode --no-ln --no-mixed"
+    bench_args = ("--steps 2 --warmup 1 --no-cpu --no-fp16 --no-decode --no-ln --no-mixed "
+                  "--no-asym")
     rec = {
         "kernel": "qgemm_prefill_kernel<256,256,128,4,2,2,1>",
         "workload": f"{wl.name} ({wl.M} tokens; " + ", ".join(L.name for L in wl.layers) + ")",
@@ -534,6 +559,8 @@ def main():
         log(f"fp16 linear stack {fb['ms_per_stack']:.3f} ms ({fb['tflops']:.0f} TFLOPs)")
     if not args.no_mixed:
         result["mixed_block"] = mixed_block_report(torch, ot, wl, layers, args.iters)
+    if not args.no_asym:
+        result["asym_weights"] = asym_report(torch, ot, wl, layers, args.iters)
     if not args.no_cpu:
         from oracle import ot_oracle
         result["cpu_baseline"] = cpu_baseline(ot_oracle, layers, M)

@@ -176,20 +176,26 @@ __device__ __forceinline__ void prefill_body(
   for (int f = 0; f < C::kFN; ++f)
 #pragma unroll
     for (int g = 0; g < C::kFM; ++g) acc[f][g] = v16i{};
-  // asymmetric weights: each lane also sums the token bytes it feeds to the
-  // matrix cores (its token fr, half fh of every K step)
+  // asymmetric weights: the code sum of every token.  The WN waves that
+  // share a token block split the work by K step (wave wn takes the steps s
+  // with s mod WN = wn) and sum the token fragments they already hold (a
+  // lane covers its token fr, half fh of the step); the partials meet in
+  // LDS after the loop.
+  static_assert(EPI != kEpiAsym || C::kKSteps % WN == 0, "K steps split over the WN waves");
   int rs[C::kFM];
 #pragma unroll
   for (int g = 0; g < C::kFM; ++g) rs[g] = 0;
-  auto mfmas = [&](int buf) {
+  auto mfmas = [&](int buf, int step) {
 #pragma unroll
     for (int f = 0; f < C::kFN; ++f)
 #pragma unroll
       for (int g = 0; g < C::kFM; ++g)
         acc[f][g] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fa[buf][f], fb[buf][g], acc[f][g], 0, 0, 0);
     if constexpr (EPI == kEpiAsym) {
+      if (step % WN == __builtin_amdgcn_readfirstlane(wn)) {
 #pragma unroll
-      for (int g = 0; g < C::kFM; ++g) rs[g] = byte_sum16(fb[buf][g], rs[g]);
+        for (int g = 0; g < C::kFM; ++g) rs[g] = byte_sum16(fb[buf][g], rs[g]);
+      }
     }
   };
 
@@ -208,7 +214,7 @@ __device__ __forceinline__ void prefill_body(
 #pragma unroll
     for (int s = 0; s + 1 < C::kKSteps; ++s) {
       read_frags(kt, s + 1, (s + 1) & 1);
-      mfmas(s & 1);
+      mfmas(s & 1, s);
       // keep the next step's fragment reads spread over this step's MFMAs
       sched_interleave<C::kFN + C::kFM, C::kFN * C::kFM, 0>();
     }
@@ -224,24 +230,48 @@ __device__ __forceinline__ void prefill_body(
     lds_barrier();
     issue_tile(kt + S);
     read_frags(kt + 1, 0, 0);
-    mfmas(1);
+    mfmas(1, C::kKSteps - 1);
     sched_interleave<C::kFN + C::kFM, C::kFN * C::kFM, C::kLoads>();
   }
   wait_vmcnt<0>();
+
+  if constexpr (EPI == kEpiAsym) {
+    // combine the two K halves of each step (lanes l and l ^ 32), then the
+    // WN waves' step subsets through LDS (the ring is idle after the loop)
+    int *part = reinterpret_cast<int *>(smem);  // [kWaves][kFM][32]
+    static_assert(C::kWaves * C::kFM * 32 * 4 <= S * C::kStage, "partials fit the ring");
+#pragma unroll
+    for (int g = 0; g < C::kFM; ++g) rs[g] += __shfl_xor(rs[g], 32);
+    __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): this wave's last fragment reads
+    lds_barrier();                        // every wave is done with the ring
+    if (lane < 32) {
+#pragma unroll
+      for (int g = 0; g < C::kFM; ++g) part[(wave * C::kFM + g) * 32 + lane] = rs[g];
+    }
+    __builtin_amdgcn_s_waitcnt(0xC07F);
+    lds_barrier();
+#pragma unroll
+    for (int g = 0; g < C::kFM; ++g) {
+      int t = 0;
+#pragma unroll
+      for (int w = 0; w < WN; ++w) t += part[((wm * WN + w) * C::kFM + g) * 32 + fr];
+      rs[g] = t;
+    }
+    __builtin_amdgcn_s_waitcnt(0xC07F);
+    lds_barrier();  // the partials are read before the ring is reused
+  }
 
   // ---- epilogue ----------------------------------------------------------------
   // 32x32 output block, 16 values per lane: lane l holds column (l mod 32)
   // and rows 8*(r/4) + 4*(l/32) + (r mod 4) for register r.  Columns are
   // tokens here and rows are channels, so registers 4j..4j+3 are four
   // consecutive channels of one token.
-  // token scales of this lane's tokens (per-token path), and the full code
-  // sums of its tokens (asymmetric weights: the two K halves meet)
+  // token scales of this lane's tokens (per-token path)
   float sx[C::kFM];
 #pragma unroll
   for (int g = 0; g < C::kFM; ++g) {
     const int m = m0 + wm * C::kTM + g * 32 + fr;
     sx[g] = (EPI == kEpiToken && m < M) ? sX[m] : 0.f;
-    if constexpr (EPI == kEpiAsym) rs[g] += __shfl_xor(rs[g], 32);
   }
   if (acc_out != nullptr) {  // test path: also stores the raw accumulators
 #pragma unroll
