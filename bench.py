@@ -369,29 +369,34 @@ def traffic_record(d, workload):
         kib = [v for _, v in disp if v > 0.5 * n_copy / 1024 / 4]
         factors[c] = n_copy / 1024 / float(np.median(kib))
     per = {L.name: {"fetch_kib": [], "write_kib": []} for L in wl.layers}
-    threads = 512  # workgroup size of the prefill kernel (256x256 tiles)
+    tile_of = {}
+    threads = 512  # workgroup size of the prefill kernel (8 waves)
     for c, sub, key in (("FETCH_SIZE", "fetch", "fetch_kib"), ("WRITE_SIZE", "write", "write_kib")):
         disp = _per_dispatch(_counter_rows(os.path.join(d, sub), c), "qgemm_prefill_kernel")
         if len(disp) % len(wl.layers):
             raise SystemExit(f"{len(disp)} prefill dispatches is not a whole number of steps")
         for i, (g, v) in enumerate(disp):
             L = wl.layers[i % len(wl.layers)]
-            tiles = -(-wl.M // 256) * -(-L.N // 256)
-            if g != tiles * threads:
-                raise SystemExit(f"dispatch {i}: grid {g} is not layer {L.name}'s {tiles * threads}")
+            # the library runs 256 x 256 or 320 (channels) x 256 (tokens) tiles
+            grids = {f"{bn}x256": -(-wl.M // 256) * -(-L.N // bn) * threads for bn in (256, 320)}
+            match = [t for t, gg in grids.items() if gg == g]
+            if not match:
+                raise SystemExit(f"dispatch {i}: grid {g} fits no tile shape of layer {L.name} "
+                                 f"({grids})")
+            tile_of[L.name] = match[0]
             per[L.name][key].append(v)
     rec_layers, alg = {}, {}
     for L in wl.layers:
         f = float(np.mean(per[L.name]["fetch_kib"]))
         w = float(np.mean(per[L.name]["write_kib"]))
-        rec_layers[L.name] = {"fetch_kib": f, "write_kib": w,
+        rec_layers[L.name] = {"fetch_kib": f, "write_kib": w, "tile": tile_of[L.name],
                               "bytes": (f * factors["FETCH_SIZE"] + w * factors["WRITE_SIZE"]) * 1024}
         alg[L.name] = wl.M * L.K + L.N * L.K + 2 * wl.M * L.N + 8 * L.N
     cmd = "cd /tmp && timeout -s KILL 120 rocprofv3 --pmc {c} --output-format csv -d <out>/{sub} -o p -- python -u <repo>/bench.py {args}"
     bench_args = ("--steps 2 --warmup 1 --no-cpu --no-fp16 --no-decode --no-ln --no-mixed "
                   "--no-asym")
     rec = {
-        "kernel": "qgemm_prefill_kernel<256,256,128,4,2,2,1>",
+        "kernel": "qgemm_prefill_kernel (256x256 or 320x256 tiles, BK 128, 2 stages)",
         "workload": f"{wl.name} ({wl.M} tokens; " + ", ".join(L.name for L in wl.layers) + ")",
         "source_files": [os.path.relpath(p, ROOT) for p in PREFILL_SOURCES],
         "source_sha256": prefill_source_digest(),

@@ -1,4 +1,6 @@
 // Prefill GEMM of the quantized linear (more than 64 tokens).
+#include <atomic>
+
 #include "ot_gemm_common.h"
 
 namespace ot {
@@ -288,83 +290,100 @@ __device__ __forceinline__ void prefill_body(
       }
     return;
   }
-  // Dequantize into a wave-private fp16 tile [kTM tokens][kTN channels] in
-  // the now idle LDS ring, then write whole token rows with 16-byte stores.
-  // In LDS the 8-byte unit u (4 channels) of token row m sits at unit
-  // u ^ (m mod U), U = kTN/4 units per row (a power of two): the lanes that
-  // write one register group (32 tokens, same channels) then spread over
-  // the banks.
-  constexpr int kUnits = C::kTN / 4;
-  static_assert((kUnits & (kUnits - 1)) == 0 && kUnits >= 16, "row of a power-of-two units");
-  static_assert(C::kWaves * C::kTM * C::kTN * 2 <= S * C::kStage, "epilogue tile fits the ring");
+  // Dequantize into a wave-private fp16 staging tile in the now idle LDS
+  // ring, then write whole token rows with 16-byte stores.  The tile holds
+  // kSlab token rows by kTN channels: the wave's whole block when every
+  // wave's block fits the ring, else 32 tokens (one register block g) at a
+  // time.  In LDS the 8-byte unit u (4 channels) of staging row r sits at
+  // unit u ^ h(r), h(r) < kSwz: the lanes that write one register group (32
+  // tokens, same channels) then spread over the banks (h(r) = r mod 16 for
+  // 128-byte rows, (r / 2) mod 8 for 320-byte rows, each checked
+  // conflict-free for 32 and 64 banks).
+  constexpr int kUnits = C::kTN / 4;                       // 8-byte units per row
+  constexpr int kSwz = (kUnits % 16 == 0) ? 16 : 8;         // XOR group of the swizzle
+  constexpr int kCpr = C::kTN / 8;                          // 16-byte chunks per row
+  constexpr bool kWhole = C::kWaves * C::kTM * C::kTN * 2 <= S * C::kStage;
+  constexpr int kSlab = kWhole ? C::kTM : 32;               // token rows per staging pass
+  constexpr int kSlabG = kSlab / 32;                        // register blocks per pass
+  static_assert(kUnits % kSwz == 0, "the swizzle permutes whole groups of units");
+  static_assert(C::kWaves * kSlab * C::kTN * 2 <= S * C::kStage, "staging tile fits the ring");
+  static_assert((kSlab * kCpr) % 64 == 0, "row pass covers the slab in whole wave passes");
+  auto stage_swz = [](int r) { return kSwz == 16 ? (r & 15) : ((r >> 1) & 7); };
   __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): this wave's last reads
   wait_vmcnt<0>();                     // the trailing out-of-range tiles
   lds_barrier();                        // every wave is done with the ring
-  uint16_t *tile = reinterpret_cast<uint16_t *>(smem) + wave * (C::kTM * C::kTN);
+  uint16_t *tile = reinterpret_cast<uint16_t *>(smem) + wave * (kSlab * C::kTN);
   const int nw0 = n0 + wn * C::kTN;   // first channel of this wave
   const int mw0 = m0 + wm * C::kTM;   // first token of this wave
-#pragma unroll
-  for (int f = 0; f < C::kFN; ++f)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int nl = f * 32 + 8 * j + 4 * fh;  // channel within the wave tile
-      const int n = nw0 + nl;
-      float4 s4 = make_float4(0.f, 0.f, 0.f, 0.f), b4 = s4;
-      if (n + 3 < N && (N & 3) == 0) {
-        s4 = *reinterpret_cast<const float4 *>(sW + n);
-        b4 = *reinterpret_cast<const float4 *>(bp + n);
-      } else {
-        if (n + 0 < N) { s4.x = sW[n + 0]; b4.x = bp[n + 0]; }
-        if (n + 1 < N) { s4.y = sW[n + 1]; b4.y = bp[n + 1]; }
-        if (n + 2 < N) { s4.z = sW[n + 2]; b4.z = bp[n + 2]; }
-        if (n + 3 < N) { s4.w = sW[n + 3]; b4.w = bp[n + 3]; }
-      }
-      const int4 z4 = load_zw4<EPI>(zW, n, N);
-#pragma unroll
-      for (int g = 0; g < C::kFM; ++g) {
-        const int ml = g * 32 + fr;
-        uint2 h;
-        const int a0 = acc[f][g][4 * j + 0] - z4.x * rs[g];
-        const int a1 = acc[f][g][4 * j + 1] - z4.y * rs[g];
-        const int a2 = acc[f][g][4 * j + 2] - z4.z * rs[g];
-        const int a3 = acc[f][g][4 * j + 3] - z4.w * rs[g];
-        h.x = (uint32_t)dequant_x<EPI>(a0, sx[g], s4.x, b4.x) |
-              ((uint32_t)dequant_x<EPI>(a1, sx[g], s4.y, b4.y) << 16);
-        h.y = (uint32_t)dequant_x<EPI>(a2, sx[g], s4.z, b4.z) |
-              ((uint32_t)dequant_x<EPI>(a3, sx[g], s4.w, b4.w) << 16);
-        const int unit = (nl >> 2) ^ (ml & (kUnits - 1));
-        *reinterpret_cast<uint2 *>(tile + ml * C::kTN + unit * 4) = h;
-      }
-    }
-  __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): the tile is in LDS
-  __builtin_amdgcn_wave_barrier();
-  // Row pass: a lane moves 8 channels (16 bytes); kTN/8 lanes cover a row.
-  constexpr int kLanesPerRow = C::kTN / 8;
-  constexpr int kRowsPerPass = 64 / kLanesPerRow;
-  const int pu = lane % kLanesPerRow;   // 16-byte unit pair in the row
-  const int prow = lane / kLanesPerRow;
   const bool vec_ok = (N & 7) == 0;
-#pragma unroll 4
-  for (int r0 = 0; r0 < C::kTM; r0 += kRowsPerPass) {
-    const int ml = r0 + prow;
-    const int x = ml & (kUnits - 1);
-    const int pair = pu ^ (x >> 1);
-    uint4 v = *reinterpret_cast<const uint4 *>(tile + ml * C::kTN + pair * 8);
-    if (x & 1) {  // the two 8-byte units of the pair are stored swapped
-      const uint32_t t0 = v.x, t1 = v.y;
-      v.x = v.z; v.y = v.w; v.z = t0; v.w = t1;
-    }
-    const int64_t m = mw0 + ml;
-    const int n = nw0 + pu * 8;
-    if (m < M) {
-      uint16_t *dst = Y + m * (int64_t)N + n;
-      if (vec_ok && n + 7 < N) {
-        *reinterpret_cast<uint4 *>(dst) = v;
-      } else {
-        const uint32_t w[4] = {v.x, v.y, v.z, v.w};
-        for (int i = 0; i < 8; ++i)
-          if (n + i < N) dst[i] = (uint16_t)(w[i >> 1] >> (16 * (i & 1)));
+#pragma unroll
+  for (int g0 = 0; g0 < C::kFM; g0 += kSlabG) {
+#pragma unroll
+    for (int f = 0; f < C::kFN; ++f)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int nl = f * 32 + 8 * j + 4 * fh;  // channel within the wave tile
+        const int n = nw0 + nl;
+        float4 s4 = make_float4(0.f, 0.f, 0.f, 0.f), b4 = s4;
+        if (n + 3 < N && (N & 3) == 0) {
+          s4 = *reinterpret_cast<const float4 *>(sW + n);
+          b4 = *reinterpret_cast<const float4 *>(bp + n);
+        } else {
+          if (n + 0 < N) { s4.x = sW[n + 0]; b4.x = bp[n + 0]; }
+          if (n + 1 < N) { s4.y = sW[n + 1]; b4.y = bp[n + 1]; }
+          if (n + 2 < N) { s4.z = sW[n + 2]; b4.z = bp[n + 2]; }
+          if (n + 3 < N) { s4.w = sW[n + 3]; b4.w = bp[n + 3]; }
+        }
+        const int4 z4 = load_zw4<EPI>(zW, n, N);
+#pragma unroll
+        for (int gs = 0; gs < kSlabG; ++gs) {
+          const int g = g0 + gs;
+          const int r = gs * 32 + fr;  // staging row
+          uint2 h;
+          const int a0 = acc[f][g][4 * j + 0] - z4.x * rs[g];
+          const int a1 = acc[f][g][4 * j + 1] - z4.y * rs[g];
+          const int a2 = acc[f][g][4 * j + 2] - z4.z * rs[g];
+          const int a3 = acc[f][g][4 * j + 3] - z4.w * rs[g];
+          h.x = (uint32_t)dequant_x<EPI>(a0, sx[g], s4.x, b4.x) |
+                ((uint32_t)dequant_x<EPI>(a1, sx[g], s4.y, b4.y) << 16);
+          h.y = (uint32_t)dequant_x<EPI>(a2, sx[g], s4.z, b4.z) |
+                ((uint32_t)dequant_x<EPI>(a3, sx[g], s4.w, b4.w) << 16);
+          const int unit = (nl >> 2) ^ stage_swz(r);
+          *reinterpret_cast<uint2 *>(tile + r * C::kTN + unit * 4) = h;
+        }
       }
+    __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): the slab is in LDS
+    __builtin_amdgcn_wave_barrier();
+    // Row pass: lane c of the slab moves 16-byte chunk c mod kCpr (8
+    // channels) of staging row c / kCpr; consecutive lanes write
+    // consecutive chunks of a token row.
+#pragma unroll 2
+    for (int c0 = 0; c0 < kSlab * kCpr; c0 += 64) {
+      const int c = c0 + lane;
+      const int r = c / kCpr, cc = c % kCpr;
+      const int x = stage_swz(r);
+      const int pair = cc ^ (x >> 1);  // units 2cc and 2cc+1 sit in this aligned pair
+      uint4 v = *reinterpret_cast<const uint4 *>(tile + r * C::kTN + pair * 8);
+      if (x & 1) {  // the two 8-byte units of the pair are stored swapped
+        const uint32_t t0 = v.x, t1 = v.y;
+        v.x = v.z; v.y = v.w; v.z = t0; v.w = t1;
+      }
+      const int64_t m = mw0 + g0 * 32 + r;
+      const int n = nw0 + cc * 8;
+      if (m < M) {
+        uint16_t *dst = Y + m * (int64_t)N + n;
+        if (vec_ok && n + 7 < N) {
+          *reinterpret_cast<uint4 *>(dst) = v;
+        } else {
+          const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+          for (int i = 0; i < 8; ++i)
+            if (n + i < N) dst[i] = (uint16_t)(w[i >> 1] >> (16 * (i & 1)));
+        }
+      }
+    }
+    if (g0 + kSlabG < C::kFM) {
+      __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): the slab is read before it is rewritten
+      __builtin_amdgcn_wave_barrier();
     }
   }
 
@@ -407,12 +426,52 @@ hipError_t launch_prefill(const int8_t *Xq, const int8_t *Wq, const float *sX, c
 
 using namespace detail;
 
-// One tile shape for every prefill layer: 256x256 output tiles, BK = 128,
-// 8 waves as 4 (weight rows) x 2 (tokens), a 2-stage ring (128 KiB of LDS).
+// Compute units of the current device (queried once per device).
+static int device_cus() {
+  static std::atomic<int> cached[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  int n = cached[dev].load(std::memory_order_relaxed);
+  if (n <= 0) {
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+      n = 256;
+    cached[dev].store(n, std::memory_order_relaxed);
+  }
+  return n;
+}
+
+// Relative time of a launch with BN x BM tiles, one workgroup per CU: whole
+// passes over the CUs, each as long as one tile.  A tile's time is
+// proportional to its products (the matrix cores run power-limited, so the
+// wider tile is no cheaper per product) over K plus its epilogue, which
+// costs about as much as 820 more K steps (measured on MI355X); the wider
+// tile carries a 2 % penalty so that ties keep the 256 x 256 tile.
+static double prefill_cost(int64_t M, int64_t N, int64_t K, int bn, int bm, int cus) {
+  const int64_t tiles = ((M + bm - 1) / bm) * ((N + bn - 1) / bn);
+  const int64_t passes = (tiles + cus - 1) / cus;
+  const double penalty = bn == 320 ? 1.02 : 1.0;
+  return (double)passes * bn * bm * ((double)K + 820.0) * penalty;
+}
+
+static bool prefill_uses_wide_tile(int64_t M, int64_t N, int64_t K) {
+  const int cus = device_cus();
+  return prefill_cost(M, N, K, 320, 256, cus) < prefill_cost(M, N, K, 256, 256, cus);
+}
+
+// Two tile shapes, both one workgroup of 8 waves per CU with a 2-stage ring
+// of BK = 128: 256 (channels) x 256 (tokens), waves 4 x 2 (128 KiB of LDS),
+// and 320 x 256, waves 2 x 4 (144 KiB).  The wider tile lets layers whose
+// tile count leaves the last pass over the CUs mostly empty fill whole
+// passes instead (4096 tokens by 5120 or 15360 channels: 256 and 768 tiles
+// of 320 x 256 against 320 and 960 of 256 x 256).  The cheaper one by
+// prefill_cost runs; both give identical results.
 hipError_t launch_qgemm_prefill(const int8_t *Xq, const int8_t *Wq, const float *sX,
                                 const int32_t *zW, const float *sW, const float *bprime,
                                 int64_t M, int64_t N, int64_t K, uint16_t *Y, int32_t *acc_out,
                                 hipStream_t st) {
+  if (prefill_uses_wide_tile(M, N, K))
+    return launch_prefill<320, 256, 128, 2, 4, 2>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y,
+                                                  acc_out, st);
   return launch_prefill<256, 256, 128, 4, 2, 2>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out,
                                                 st);
 }

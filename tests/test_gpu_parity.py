@@ -244,3 +244,34 @@ def test_pipeline_opt125m(a_bits, w_bits):
     assert np.array_equal(host(Wq), ref["Wq"])
     assert np.array_equal(host(acc), ref["acc"])
     assert_fp16_close(host(Y), ref["Y"])
+
+
+# --------------------------------------------------------------------------
+# Prefill tile shapes and the LDS-staged epilogue (Y only, no acc_out): the
+# library runs 256 x 256 tiles, or 320 (channels) x 256 (tokens) tiles when
+# they need fewer passes over the compute units.  On a 256-CU MI355X the
+# first shape below takes the 320-wide tile (256 tiles against 320 of
+# 256 x 256), the second the 256-wide one; both have ragged M, N and K.
+# --------------------------------------------------------------------------
+PREFILL_TILE_SHAPES = [(500, 40860, 272), (300, 1000, 1040)]
+
+
+@pytest.mark.parametrize("M,N,K", PREFILL_TILE_SHAPES)
+@pytest.mark.parametrize("flavour", ["channel", "token", "asym"])
+def test_prefill_tiles_staged_epilogue(M, N, K, flavour):
+    Xq, Wq, sW, bp = _random_qlinear_inputs(M, N, K, 8, 8, M + 3 * N + 7 * K)
+    r = np.random.default_rng(N)
+    case(f"prefill staged epilogue {flavour} M={M} N={N} K={K} "
+         f"cus={torch.cuda.get_device_properties(0).multi_processor_count}")
+    if flavour == "channel":
+        Y = ot.qlinear(dev(Xq), dev(Wq), dev(sW), dev(bp), 8, 8)
+        ref = O.epilogue(O.int_gemm(Xq, Wq), sW, bp)
+    elif flavour == "token":
+        sX = r.uniform(0.01, 0.2, size=M).astype(np.float32)
+        Y = ot.qlinear_per_token(dev(Xq), dev(Wq), dev(sX), dev(sW), dev(bp), 8, 8)
+        ref = O.epilogue_per_token(O.int_gemm(Xq, Wq), sX, sW, bp)
+    else:
+        zW = r.integers(-128, 128, size=N).astype(np.int32)
+        Y = ot.qlinear_asym(dev(Xq), dev(Wq), dev(sW), dev(zW), dev(bp), 8, 8)
+        ref = O.epilogue(O.int_gemm_asym(Xq, Wq, zW), sW, bp)
+    assert_fp16_close(host(Y), ref)
