@@ -190,8 +190,14 @@ ot_status ot_ln_quantize_act(const uint16_t *h, int64_t M, int64_t K,
  *   acc_out  NULL, or [M x N] int32 (device) that also receives acc (for
  *           testing; costs extra memory traffic).
  *   workspace  NULL, or at least ot_qlinear_workspace_size(M, N, K) bytes of
- *           device memory the call may use as scratch; with NULL the call
- *           uses no scratch memory.  Results do not depend on it.
+ *           16-byte-aligned device memory the call may use as scratch; with
+ *           NULL the call uses no scratch memory.  Results do not depend on
+ *           it.  For 17..64 tokens and at most 32 output channels per compute
+ *           unit the call then splits K over more workgroups and adds their
+ *           int32 partial sums in a second kernel (the sums are exact, so the
+ *           outputs are identical).  The contents need no initialization and
+ *           are left unspecified; calls that overlap in time must not share
+ *           a workspace.
  *
  * Asynchronous on stream; no synchronization, no allocation.
  */
@@ -280,7 +286,9 @@ ot_status ot_qlinear_per_token(const int8_t *Xq, const int8_t *Wq,
                                int64_t K, int a_bits, int w_bits, uint16_t *Y,
                                int32_t *acc_out, void *workspace, void *stream);
 
-/* Bytes of optional scratch ot_qlinear can use for these sizes (0 if none). */
+/* Bytes of optional scratch that ot_qlinear, ot_qlinear_per_token and
+ * ot_qlinear_asym can use for these sizes on the current device (0 if none;
+ * also 0 for sizes the calls reject).  Synchronous, no device work. */
 size_t ot_qlinear_workspace_size(int64_t M, int64_t N, int64_t K);
 
 #ifdef __cplusplus

@@ -134,7 +134,6 @@ ot_status ot_ln_quantize_act(const uint16_t *h, int64_t M, int64_t K, const uint
 ot_status ot_qlinear(const int8_t *Xq, const int8_t *Wq, const float *sW, const float *bprime,
                      int64_t M, int64_t N, int64_t K, int a_bits, int w_bits, uint16_t *Y,
                      int32_t *acc_out, void *workspace, void *stream) {
-  (void)workspace;
   if (!bits_ok(a_bits) || !bits_ok(w_bits) || M < 0 || N < 0 || K < 0) return OT_EINVAL;
   if (N == 0 || K < 16 || K % 16 != 0 || K > kMaxK || M > kMaxRows || N > kMaxRows)
     return OT_ESHAPE;
@@ -143,10 +142,11 @@ ot_status ot_qlinear(const int8_t *Xq, const int8_t *Wq, const float *sW, const 
   if (M == 0) return OT_OK;
   if (!Xq || !Wq || !sW || !bprime || !Y) return OT_EINVAL;
   if (!aligned16(Xq) || !aligned16(Wq) || !aligned16(sW) || !aligned16(bprime) || !aligned16(Y) ||
-      (acc_out && !aligned16(acc_out)))
+      (acc_out && !aligned16(acc_out)) ||
+      (workspace && !aligned16(workspace)))
     return OT_EINVAL;
   return hip_status(ot::launch_qgemm(Xq, Wq, nullptr, nullptr, sW, bprime, M, N, K, Y, acc_out,
-                                     static_cast<hipStream_t>(stream)));
+                                     workspace, static_cast<hipStream_t>(stream)));
 }
 
 ot_status ot_quantize_act_per_token(const uint16_t *x, int64_t M, int64_t K, int a_bits,
@@ -178,7 +178,6 @@ ot_status ot_qlinear_per_token(const int8_t *Xq, const int8_t *Wq, const float *
                                const float *sW, const float *bprime, int64_t M, int64_t N,
                                int64_t K, int a_bits, int w_bits, uint16_t *Y, int32_t *acc_out,
                                void *workspace, void *stream) {
-  (void)workspace;
   if (!bits_ok(a_bits) || !bits_ok(w_bits) || M < 0 || N < 0 || K < 0) return OT_EINVAL;
   if (N == 0 || K < 16 || K % 16 != 0 || K > kMaxK || M > kMaxRows || N > kMaxRows)
     return OT_ESHAPE;
@@ -187,10 +186,11 @@ ot_status ot_qlinear_per_token(const int8_t *Xq, const int8_t *Wq, const float *
   if (M == 0) return OT_OK;
   if (!Xq || !Wq || !sX || !sW || !bprime || !Y) return OT_EINVAL;
   if (!aligned16(Xq) || !aligned16(Wq) || !aligned16(sW) || !aligned16(bprime) || !aligned16(Y) ||
-      (acc_out && !aligned16(acc_out)))
+      (acc_out && !aligned16(acc_out)) ||
+      (workspace && !aligned16(workspace)))
     return OT_EINVAL;
   return hip_status(ot::launch_qgemm(Xq, Wq, sX, nullptr, sW, bprime, M, N, K, Y, acc_out,
-                                     static_cast<hipStream_t>(stream)));
+                                     workspace, static_cast<hipStream_t>(stream)));
 }
 
 ot_status ot_fold_weights_asym(const uint16_t *W, const uint16_t *b, int64_t N, int64_t K,
@@ -211,7 +211,6 @@ ot_status ot_qlinear_asym(const int8_t *Xq, const int8_t *Wq, const float *sW, c
                           const float *bprime, int64_t M, int64_t N, int64_t K, int a_bits,
                           int w_bits, uint16_t *Y, int32_t *acc_out, void *workspace,
                           void *stream) {
-  (void)workspace;
   if (!bits_ok(a_bits) || !bits_ok(w_bits) || M < 0 || N < 0 || K < 0) return OT_EINVAL;
   if (N == 0 || K < 16 || K % 16 != 0 || K > kMaxK || M > kMaxRows || N > kMaxRows)
     return OT_ESHAPE;
@@ -222,17 +221,16 @@ ot_status ot_qlinear_asym(const int8_t *Xq, const int8_t *Wq, const float *sW, c
   if (M == 0) return OT_OK;
   if (!Xq || !Wq || !sW || !zW || !bprime || !Y) return OT_EINVAL;
   if (!aligned16(Xq) || !aligned16(Wq) || !aligned16(sW) || !aligned16(zW) ||
-      !aligned16(bprime) || !aligned16(Y) || (acc_out && !aligned16(acc_out)))
+      !aligned16(bprime) || !aligned16(Y) || (acc_out && !aligned16(acc_out)) ||
+      (workspace && !aligned16(workspace)))
     return OT_EINVAL;
   return hip_status(ot::launch_qgemm(Xq, Wq, nullptr, zW, sW, bprime, M, N, K, Y, acc_out,
-                                     static_cast<hipStream_t>(stream)));
+                                     workspace, static_cast<hipStream_t>(stream)));
 }
 
 size_t ot_qlinear_workspace_size(int64_t M, int64_t N, int64_t K) {
-  (void)M;
-  (void)N;
-  (void)K;
-  return 0;
+  if (M <= 0 || N <= 0 || K <= 0 || M > kMaxRows || N > kMaxRows || K > kMaxK) return 0;
+  return ot::qgemm_workspace_bytes(M, N, K);
 }
 
 }  // extern "C"

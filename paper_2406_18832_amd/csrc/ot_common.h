@@ -34,6 +34,10 @@ __device__ inline uint16_t float_to_half_bits(float f) {
   return __builtin_bit_cast(uint16_t, (_Float16)f);
 }
 
+// Compute units of the current device (queried once per device; 256 if the
+// query fails).  The GEMM launchers size their grids by it.
+int device_cus();
+
 // Launchers: each validates nothing (the C ABI layer does) and returns the
 // launch status.
 hipError_t launch_calib_reset(float *minmax, int64_t K, hipStream_t st);
@@ -52,16 +56,20 @@ hipError_t launch_ln_quantize_act(const uint16_t *h, int64_t M, int64_t K, const
 hipError_t launch_qgemm_decode(const int8_t *Xq, const int8_t *Wq, const float *sX,
                                const int32_t *zW, const float *sW, const float *bprime,
                                int64_t M, int64_t N, int64_t K, uint16_t *Y, int32_t *acc_out,
-                               hipStream_t st);
+                               void *workspace, hipStream_t st);
+// Scratch bytes the decode kernels use for split-K partial sums (0: none).
+size_t qgemm_decode_workspace_bytes(int64_t M, int64_t N, int64_t K);
 hipError_t launch_qgemm_prefill(const int8_t *Xq, const int8_t *Wq, const float *sX,
                                 const int32_t *zW, const float *sW, const float *bprime,
                                 int64_t M, int64_t N, int64_t K, uint16_t *Y, int32_t *acc_out,
                                 hipStream_t st);
 // Epilogue: sX != nullptr per-token scales (Eq. (c)); zW != nullptr
 // asymmetric weight zero points (Eq. (a)); neither, per-channel (Eq. (g)).
+// workspace: nullptr, or at least qgemm_workspace_bytes(M, N, K) bytes.
 hipError_t launch_qgemm(const int8_t *Xq, const int8_t *Wq, const float *sX, const int32_t *zW,
                         const float *sW, const float *bprime, int64_t M, int64_t N, int64_t K,
-                        uint16_t *Y, int32_t *acc_out, hipStream_t st);
+                        uint16_t *Y, int32_t *acc_out, void *workspace, hipStream_t st);
+size_t qgemm_workspace_bytes(int64_t M, int64_t N, int64_t K);
 hipError_t launch_fold_asym(const uint16_t *W, const uint16_t *b, int64_t N, int64_t K,
                             int w_bits, const float *z, const float *s, int8_t *Wq, float *sW,
                             int32_t *zW, float *bprime, hipStream_t st);

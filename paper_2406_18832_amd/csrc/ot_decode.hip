@@ -1,5 +1,7 @@
 // Decode GEMM of the quantized linear (at most 64 tokens), bound by
 // streaming the weights from HBM.
+#include <algorithm>
+
 #include "ot_gemm_common.h"
 
 namespace ot {
@@ -50,12 +52,18 @@ __device__ __forceinline__ int swz_rows(int r) {
   else return r & 15;
 }
 
-template <int MB, int NR, int NK, int RBW, int BKD, int S, int EPI>
+// Split K (SPLIT): workgroup (x, y) takes the y-th run of `per` stages of K
+// and, instead of the epilogue, writes its integer partial sums to
+// part[y][m][n] (and, for asymmetric weights, the tokens' partial code sums
+// to part_rs[y][m] from the first row tile); decode_reduce_kernel adds the
+// runs and applies the epilogue.
+template <int MB, int NR, int NK, int RBW, int BKD, int S, int EPI, bool SPLIT>
 __device__ __forceinline__ void decode_body(
     int8_t *smem, const int8_t *__restrict__ Xq, const int8_t *__restrict__ Wq,
     const float *__restrict__ sX, const int32_t *__restrict__ zW, const float *__restrict__ sW,
     const float *__restrict__ bp, int M, int N, int K, uint16_t *__restrict__ Y,
-    int32_t *__restrict__ acc_out) {
+    int32_t *__restrict__ acc_out, int32_t *__restrict__ part, int32_t *__restrict__ part_rs,
+    int per) {
   using C = DecodeCfg<MB, NR, NK, RBW, BKD, S>;
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -79,10 +87,15 @@ __device__ __forceinline__ void decode_body(
     const int grow = row < C::kTokRows ? row : row - C::kTokRows;
     goff[j] = (uint32_t)(grow * K + ch * 16);
   }
-  const int nst = (K + BKD - 1) / BKD;
+  // stages [st0, st0 + nst) of K; a split never starts past the last stage
+  int st0 = 0, nst = (K + BKD - 1) / BKD;
+  if constexpr (SPLIT) {
+    st0 = blockIdx.y * per;
+    nst = min(nst - st0, per);
+  }
   auto issue = [&](int st) {
     int8_t *dst = smem + (st % S) * C::kStage;
-    const int k0 = st * BKD;
+    const int k0 = (st0 + st) * BKD;  // stages past this split's run are loaded but unused
 #pragma unroll
     for (int j = 0; j < C::kLoads; ++j) {
       const int q = wave * C::kLoads + j;  // wave-uniform
@@ -201,6 +214,27 @@ __device__ __forceinline__ void decode_body(
   }
 
   // 16x16 output blocks: lane l holds token l%16 and channels 4*(l/16) + r
+  if constexpr (SPLIT) {
+    const int64_t slab = (int64_t)blockIdx.y * M;
+#pragma unroll
+    for (int j = 0; j < MB; ++j) {
+      const int m = j * 16 + r16;
+      if (m >= M) continue;
+#pragma unroll
+      for (int i = 0; i < RBW; ++i) {
+        const int64_t n = nwg0 + (rg * RBW + i) * 16 + 4 * c4;
+        int32_t *dst = part + (slab + m) * N + n;
+        if (n + 3 < N && (N & 3) == 0) {
+          *reinterpret_cast<v4i *>(dst) = acc[i][j];
+        } else {
+          for (int e = 0; e < 4; ++e)
+            if (n + e < N) dst[e] = acc[i][j][e];
+        }
+      }
+      if (EPI == kEpiAsym && blockIdx.x == 0 && rg == 0 && c4 == 0) part_rs[slab + m] = rs[j];
+    }
+    return;
+  }
 #pragma unroll
   for (int j = 0; j < MB; ++j) {
     const int m = j * 16 + r16;
@@ -221,7 +255,79 @@ __global__ __launch_bounds__(64 * NR * NK) void qgemm_decode_kernel(
     int M, int N, int K, uint16_t *__restrict__ Y, int32_t *__restrict__ acc_out) {
   __shared__ __attribute__((aligned(1024)))
   int8_t smem[S * DecodeCfg<MB, NR, NK, RBW, BKD, S>::kStage];
-  decode_body<MB, NR, NK, RBW, BKD, S, EPI>(smem, Xq, Wq, sX, zW, sW, bp, M, N, K, Y, acc_out);
+  decode_body<MB, NR, NK, RBW, BKD, S, EPI, false>(smem, Xq, Wq, sX, zW, sW, bp, M, N, K, Y,
+                                                   acc_out, nullptr, nullptr, 0);
+}
+
+// Split-K partial sums (ROWSUM: also the token code sums of asymmetric weights).
+template <int MB, int NR, int NK, int RBW, int BKD, int S, bool ROWSUM>
+__global__ __launch_bounds__(64 * NR * NK) void qgemm_decode_split_kernel(
+    const int8_t *__restrict__ Xq, const int8_t *__restrict__ Wq, int M, int N, int K,
+    int32_t *__restrict__ part, int32_t *__restrict__ part_rs, int per) {
+  __shared__ __attribute__((aligned(1024)))
+  int8_t smem[S * DecodeCfg<MB, NR, NK, RBW, BKD, S>::kStage];
+  decode_body<MB, NR, NK, RBW, BKD, S, ROWSUM ? kEpiAsym : kEpiChannel, true>(
+      smem, Xq, Wq, nullptr, nullptr, nullptr, nullptr, M, N, K, nullptr, nullptr, part, part_rs,
+      per);
+}
+
+// Adds the split runs' partial sums (in run order; integer sums, so any order
+// gives the same result) and applies the epilogue: thread t takes channels
+// 4 (t mod N4) .. +3 of token t / N4.
+template <int EPI>
+__global__ __launch_bounds__(256) void decode_reduce_kernel(
+    const int32_t *__restrict__ part, const int32_t *__restrict__ part_rs, int splits,
+    const float *__restrict__ sX, const int32_t *__restrict__ zW, const float *__restrict__ sW,
+    const float *__restrict__ bp, int M, int N, uint16_t *__restrict__ Y,
+    int32_t *__restrict__ acc_out) {
+  const int n4 = (N + 3) / 4;
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (t >= (int64_t)M * n4) return;
+  const int m = (int)(t / n4), n = 4 * (int)(t % n4);
+  int a[4] = {0, 0, 0, 0};
+  int rs = 0;
+  for (int s = 0; s < splits; ++s) {
+    const int32_t *src = part + ((int64_t)s * M + m) * N + n;
+    if (n + 3 < N && (N & 3) == 0) {
+      const v4i v = *reinterpret_cast<const v4i *>(src);
+      a[0] += v[0]; a[1] += v[1]; a[2] += v[2]; a[3] += v[3];
+    } else {
+      for (int e = 0; e < 4; ++e)
+        if (n + e < N) a[e] += src[e];
+    }
+    if constexpr (EPI == kEpiAsym) rs += part_rs[(int64_t)s * M + m];
+  }
+  const float sx = EPI == kEpiToken ? sX[m] : 0.f;
+  store4<EPI>(Y, acc_out, sW, bp, zW, sx, rs, m, n, M, N, a[0], a[1], a[2], a[3]);
+}
+
+template <int MB, int NR, int NK, int RBW, int BKD, int S>
+hipError_t launch_decode_split(const int8_t *Xq, const int8_t *Wq, const float *sX,
+                               const int32_t *zW, const float *sW, const float *bp, int64_t M,
+                               int64_t N, int64_t K, uint16_t *Y, int32_t *acc_out, int splits,
+                               int per, int32_t *part, int32_t *part_rs, hipStream_t st) {
+  constexpr int rows = 16 * RBW * NR;
+  const dim3 grid((unsigned)((N + rows - 1) / rows), (unsigned)splits);
+  const dim3 block(64 * NR * NK);
+  if (zW)
+    qgemm_decode_split_kernel<MB, NR, NK, RBW, BKD, S, true><<<grid, block, 0, st>>>(
+        Xq, Wq, (int)M, (int)N, (int)K, part, part_rs, per);
+  else
+    qgemm_decode_split_kernel<MB, NR, NK, RBW, BKD, S, false><<<grid, block, 0, st>>>(
+        Xq, Wq, (int)M, (int)N, (int)K, part, part_rs, per);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const unsigned rgrid = (unsigned)((M * ((N + 3) / 4) + 255) / 256);
+  if (sX)
+    decode_reduce_kernel<kEpiToken><<<rgrid, 256, 0, st>>>(part, part_rs, splits, sX, zW, sW, bp,
+                                                            (int)M, (int)N, Y, acc_out);
+  else if (zW)
+    decode_reduce_kernel<kEpiAsym><<<rgrid, 256, 0, st>>>(part, part_rs, splits, sX, zW, sW, bp,
+                                                           (int)M, (int)N, Y, acc_out);
+  else
+    decode_reduce_kernel<kEpiChannel><<<rgrid, 256, 0, st>>>(part, part_rs, splits, sX, zW, sW,
+                                                              bp, (int)M, (int)N, Y, acc_out);
+  return hipGetLastError();
 }
 
 // Epilogue by argument: sX != nullptr per-token scales sX [M]; zW != nullptr
@@ -249,30 +355,75 @@ hipError_t launch_decode(const int8_t *Xq, const int8_t *Wq, const float *sX, co
 
 using namespace detail;
 
+// Split K for 17-64 tokens: with at most 32 weight rows per CU the 128-row
+// tiles that keep the token re-reads low leave CUs idle, so each row tile's
+// K is cut into runs of whole 256-byte stages (at least 4 per run, at most
+// 8 runs) that fill the CUs; a second kernel adds the runs' int32 partial
+// sums (splits x M x N, plus splits x M token code sums) and applies the
+// epilogue.  Returns the number of runs, 1 for no split.
+static int decode_splits(int64_t M, int64_t N, int64_t K, int64_t cus, int *per_out) {
+  constexpr int kRows = 128, kBKD = 256;
+  if (M <= 16 || M > 64 || N > 32 * cus) return 1;
+  const int64_t tiles = (N + kRows - 1) / kRows;
+  const int64_t nst = (K + kBKD - 1) / kBKD;
+  int64_t sp = std::min<int64_t>(std::min<int64_t>(cus / tiles, nst / 4), 8);
+  if (sp < 2) return 1;
+  const int64_t per = (nst + sp - 1) / sp;  // stages per run; no run is empty
+  if (per_out) *per_out = (int)per;
+  return (int)((nst + per - 1) / per);
+}
+
+size_t qgemm_decode_workspace_bytes(int64_t M, int64_t N, int64_t K) {
+  const int sp = decode_splits(M, N, K, device_cus(), nullptr);
+  return sp > 1 ? (size_t)sp * (size_t)M * (size_t)(N + 1) * sizeof(int32_t) : 0;
+}
+
 hipError_t launch_qgemm_decode(const int8_t *Xq, const int8_t *Wq, const float *sX,
                                const int32_t *zW, const float *sW, const float *bprime,
                                int64_t M, int64_t N, int64_t K, uint16_t *Y, int32_t *acc_out,
-                               hipStream_t st) {
+                               void *workspace, hipStream_t st) {
   // Template arguments
-  // <token blocks, row groups, K groups, row blocks per wave, BKD, stages>.
-  // Up to 16 tokens the workgroup is one 16-row block split over 4 K groups
-  // (small LDS footprint, several workgroups per CU).  For 17-64 tokens a
-  // workgroup of 8 waves fills most of a CU's LDS, so one runs per CU: the
-  // tile height is the smallest of 32/64/128 rows whose grid fits in one
-  // pass over the 256 CUs (taller tiles re-read the token tile less, shorter
-  // ones use more CUs); past 128 rows x 256 CUs, 64-row tiles keep the last
-  // pass's tail short.
-  if (M <= 16) return launch_decode<1, 1, 4, 1, 256, 4>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, st);
-  constexpr int64_t kCUs = 256;
-  const int rows = N <= 32 * kCUs ? 32 : N <= 64 * kCUs ? 64 : N <= 128 * kCUs ? 128 : 64;
+  // <token blocks, row groups, K groups, row blocks per wave, BKD, stages>,
+  // chosen from a sweep of every valid configuration on the OPT-30B layers
+  // (N = 7168 .. 28672) at 1 .. 64 tokens on MI355X.
+  // Up to 16 tokens: 32-row tiles.  Where they fill at most one pass over
+  // the CUs, one 8-wave workgroup per CU streams 16 KiB of weights per stage
+  // (512-byte K slices, 3 stages ahead); with more rows, 2-wave workgroups
+  // with 128-byte slices run six to a CU.  Below 16 rows per CU, 16-row tiles
+  // split over 4 K groups.
+  // For 17-64 tokens a workgroup of 8 waves fills most of a CU's LDS, so one
+  // runs per CU: the tile height is the smallest of 32/64/128 rows whose grid
+  // fits in one pass over the CUs (taller tiles re-read the token tile less,
+  // shorter ones use more CUs); past 128 rows per CU, 64-row tiles keep the
+  // last pass's tail short.
+  const int64_t cus = device_cus();
+  int per = 0;
+  const int sp = workspace ? decode_splits(M, N, K, cus, &per) : 1;
+  if (sp > 1) {
+    int32_t *part = static_cast<int32_t *>(workspace);
+    int32_t *part_rs = part + (int64_t)sp * M * N;
+    if (M <= 32)
+      return launch_decode_split<2, 8, 1, 1, 256, 3>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y,
+                                                     acc_out, sp, per, part, part_rs, st);
+    return launch_decode_split<4, 8, 1, 1, 256, 3>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y,
+                                                   acc_out, sp, per, part, part_rs, st);
+  }
+  if (M <= 16) {
+    if (N <= 16 * cus)
+      return launch_decode<1, 1, 4, 1, 256, 4>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, st);
+    if (N <= 32 * cus)
+      return launch_decode<1, 2, 4, 1, 512, 4>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, st);
+    return launch_decode<1, 2, 1, 1, 128, 4>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, st);
+  }
+  const int rows = N <= 32 * cus ? 32 : N <= 64 * cus ? 64 : N <= 128 * cus ? 128 : 64;
   if (M <= 32) {
     if (rows == 32) return launch_decode<2, 2, 4, 1, 256, 4>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, st);
     if (rows == 64) return launch_decode<2, 4, 2, 1, 256, 3>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, st);
-    return launch_decode<2, 4, 2, 2, 256, 3>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, st);
+    return launch_decode<2, 8, 1, 1, 256, 3>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, st);
   }
   if (rows == 32) return launch_decode<4, 2, 4, 1, 256, 4>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, st);
   if (rows == 64) return launch_decode<4, 4, 2, 1, 256, 3>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, st);
-  return launch_decode<4, 4, 2, 2, 256, 3>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, st);
+  return launch_decode<4, 8, 1, 1, 256, 3>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, st);
 }
 
 }  // namespace ot

@@ -1,6 +1,4 @@
 // Prefill GEMM of the quantized linear (more than 64 tokens).
-#include <atomic>
-
 #include "ot_gemm_common.h"
 
 namespace ot {
@@ -425,20 +423,6 @@ hipError_t launch_prefill(const int8_t *Xq, const int8_t *Wq, const float *sX, c
 }  // namespace detail
 
 using namespace detail;
-
-// Compute units of the current device (queried once per device).
-static int device_cus() {
-  static std::atomic<int> cached[64];
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-  int n = cached[dev].load(std::memory_order_relaxed);
-  if (n <= 0) {
-    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
-      n = 256;
-    cached[dev].store(n, std::memory_order_relaxed);
-  }
-  return n;
-}
 
 // Relative time of a launch with BN x BM tiles, one workgroup per CU: whole
 // passes over the CUs, each as long as one tile.  A tile's time is

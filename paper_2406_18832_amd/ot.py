@@ -111,6 +111,18 @@ def _dev(t, dtype, name, shape=None):
     return t.data_ptr()
 
 
+def _dev_ws(workspace, M, N, K):
+    """Device pointer of an optional workspace, checked against the bytes the
+    library asks for at these sizes (the C ABI cannot see its size)."""
+    if workspace is None:
+        return None
+    ptr = _dev(workspace, torch.uint8, "workspace")
+    need = ot_qlinear_workspace_size(M, N, K)
+    if workspace.numel() < need:
+        raise ValueError(f"workspace holds {workspace.numel()} bytes, the call needs {need}")
+    return ptr
+
+
 def _stream(stream):
     if stream is None:
         return torch.cuda.current_stream().cuda_stream
@@ -173,7 +185,7 @@ def ot_qlinear(Xq, Wq, sW, bprime, a_bits, w_bits, Y, acc_out=None, workspace=No
     N = Wq.shape[0]
     if Wq.shape[1] != K:
         raise ValueError("Xq and Wq disagree on K")
-    ws = None if workspace is None else _dev(workspace, torch.uint8, "workspace")
+    ws = _dev_ws(workspace, M, N, K)
     rc = lib().ot_qlinear(_dev(Xq, torch.int8, "Xq"), _dev(Wq, torch.int8, "Wq"),
                           _dev(sW, torch.float32, "sW", (N,)),
                           _dev(bprime, torch.float32, "bprime", (N,)), M, N, K, int(a_bits),
@@ -247,8 +259,7 @@ def ot_qlinear_per_token(Xq, Wq, sX, sW, bprime, a_bits, w_bits, Y, acc_out=None
                                     int(a_bits), int(w_bits),
                                     _dev(Y, torch.float16, "Y", (M, N)),
                                     _dev(acc_out, torch.int32, "acc_out", (M, N)),
-                                    None if workspace is None else workspace.data_ptr(),
-                                    _stream(stream))
+                                    _dev_ws(workspace, M, N, K), _stream(stream))
     _check(rc, "ot_qlinear_per_token")
 
 
@@ -281,7 +292,7 @@ def ot_qlinear_asym(Xq, Wq, sW, zW, bprime, a_bits, w_bits, Y, acc_out=None, wor
                                _dev(bprime, torch.float32, "bprime", (N,)), M, N, K, int(a_bits),
                                int(w_bits), _dev(Y, torch.float16, "Y", (M, N)),
                                _dev(acc_out, torch.int32, "acc_out", (M, N)),
-                               None if workspace is None else workspace.data_ptr(), _stream(stream))
+                               _dev_ws(workspace, M, N, K), _stream(stream))
     _check(rc, "ot_qlinear_asym")
 
 
@@ -327,11 +338,25 @@ def ln_quantize_act(h, gamma, beta, eps, a_bits, z, inv_s):
     return Xq
 
 
-def qlinear(Xq, Wq, sW, bprime, a_bits, w_bits, want_acc=False):
+def workspace_for(M: int, N: int, K: int, device=None):
+    """A scratch buffer of ot_qlinear_workspace_size(M, N, K) bytes for the
+    quantized-linear calls, or None when they use none at these sizes."""
+    n = ot_qlinear_workspace_size(M, N, K)
+    return torch.empty(n, dtype=torch.uint8, device=device or "cuda") if n else None
+
+
+def _ws(workspace, Xq, Wq):
+    """workspace=True allocates one for the call's sizes; a tensor is used as given."""
+    if workspace is True:
+        return workspace_for(Xq.shape[0], Wq.shape[0], Xq.shape[1], Xq.device)
+    return None if workspace is None or workspace is False else workspace
+
+
+def qlinear(Xq, Wq, sW, bprime, a_bits, w_bits, want_acc=False, workspace=None):
     M, N = Xq.shape[0], Wq.shape[0]
     Y = torch.empty((M, N), dtype=torch.float16, device=Xq.device)
     acc = torch.empty((M, N), dtype=torch.int32, device=Xq.device) if want_acc else None
-    ot_qlinear(Xq, Wq, sW, bprime, a_bits, w_bits, Y, acc)
+    ot_qlinear(Xq, Wq, sW, bprime, a_bits, w_bits, Y, acc, _ws(workspace, Xq, Wq))
     return (Y, acc) if want_acc else Y
 
 
@@ -352,11 +377,11 @@ def fold_weights_per_token(W, b, zres, w_bits):
     return Wq, sW, bprime
 
 
-def qlinear_per_token(Xq, Wq, sX, sW, bprime, a_bits, w_bits, want_acc=False):
+def qlinear_per_token(Xq, Wq, sX, sW, bprime, a_bits, w_bits, want_acc=False, workspace=None):
     M, N = Xq.shape[0], Wq.shape[0]
     Y = torch.empty((M, N), dtype=torch.float16, device=Xq.device)
     acc = torch.empty((M, N), dtype=torch.int32, device=Xq.device) if want_acc else None
-    ot_qlinear_per_token(Xq, Wq, sX, sW, bprime, a_bits, w_bits, Y, acc)
+    ot_qlinear_per_token(Xq, Wq, sX, sW, bprime, a_bits, w_bits, Y, acc, _ws(workspace, Xq, Wq))
     return (Y, acc) if want_acc else Y
 
 
@@ -370,9 +395,9 @@ def fold_weights_asym(W, b, w_bits, z, s):
     return Wq, sW, zW, bprime
 
 
-def qlinear_asym(Xq, Wq, sW, zW, bprime, a_bits, w_bits, want_acc=False):
+def qlinear_asym(Xq, Wq, sW, zW, bprime, a_bits, w_bits, want_acc=False, workspace=None):
     M, N = Xq.shape[0], Wq.shape[0]
     Y = torch.empty((M, N), dtype=torch.float16, device=Xq.device)
     acc = torch.empty((M, N), dtype=torch.int32, device=Xq.device) if want_acc else None
-    ot_qlinear_asym(Xq, Wq, sW, zW, bprime, a_bits, w_bits, Y, acc)
+    ot_qlinear_asym(Xq, Wq, sW, zW, bprime, a_bits, w_bits, Y, acc, _ws(workspace, Xq, Wq))
     return (Y, acc) if want_acc else Y

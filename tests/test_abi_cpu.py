@@ -33,7 +33,21 @@ def test_strerror_and_version():
     for code in range(1, 6):
         assert ot.ot_strerror(code) not in ("ok", "unknown status")
     assert ot.ot_strerror(99) == "unknown status"
-    assert ot.ot_qlinear_workspace_size(64, 4096, 4096) == 0
+
+
+def test_workspace_size_rule():
+    """Scratch only for the split-K decode path: 17..64 tokens and at most 32
+    output channels per compute unit (256 CUs without a GPU, as on MI355X);
+    runs x M x (N + 1) int32 for 2..8 runs of at least 4 K stages."""
+    ws = ot.ot_qlinear_workspace_size
+    for M, N, K in [(16, 7168, 7168), (65, 7168, 7168), (4096, 5120, 5120), (64, 21504, 7168),
+                    (64, 7168, 1024), (0, 7168, 7168), (64, 0, 7168), (64, 7168, 0)]:
+        assert ws(M, N, K) == 0, (M, N, K)
+    for M, N, K in [(17, 7168, 7168), (64, 7168, 28672), (33, 300, 4112), (64, 8192, 2048)]:
+        n = ws(M, N, K)
+        unit = M * (N + 1) * 4
+        assert n % unit == 0 and 2 <= n // unit <= 8, (M, N, K, n)
+    assert ws(64, 7168, 7168) == 4 * 64 * 7169 * 4  # 56 row tiles of 128 x 4 runs of 7 stages
 
 
 NULL = None
@@ -140,3 +154,14 @@ def test_binding_refuses_host_tensors():
     with pytest.raises(ValueError):
         ot.ot_quantize_act(x, 8, torch.zeros(32), torch.zeros(32),
                            torch.zeros((4, 32), dtype=torch.int8))
+
+
+def test_binding_workspace_argument_forms():
+    """None/False mean no workspace; a tensor passes through unchanged."""
+    import torch
+    t = torch.empty(8, dtype=torch.uint8)
+    x, w = torch.empty((2, 16), dtype=torch.int8), torch.empty((4, 16), dtype=torch.int8)
+    assert ot._ws(None, x, w) is None and ot._ws(False, x, w) is None
+    assert ot._ws(t, x, w) is t
+    with pytest.raises(ValueError):
+        ot._dev_ws(torch.empty(8, dtype=torch.uint8), 2, 4, 16)  # host tensor

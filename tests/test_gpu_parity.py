@@ -158,12 +158,16 @@ QL_SHAPES = [
     # decode kernel (M <= 64)
     (1, 8, 16), (1, 300, 1040), (5, 772, 768), (16, 256, 4096), (17, 100, 400),
     (32, 513, 128), (33, 64, 48), (64, 1000, 2064),
-    # decode kernel, every tile height for 17-64 tokens (32 rows up to
-    # N = 8192, 64 rows up to 16384, 128 rows up to 32768, 64 rows beyond),
-    # on both sides of each boundary, with ragged N and K tails
+    # decode kernel, every tile for up to 16 tokens (16-row tiles up to
+    # N = 4096, 32-row tiles with 512-byte K slices up to 8192, 32-row tiles
+    # with 128-byte slices beyond) and every tile height for 17-64 tokens (32
+    # rows up to N = 8192, 64 rows up to 16384, 128 rows up to 32768, 64 rows
+    # beyond), on both sides of each boundary, with ragged N and K tails
+    (1, 4096, 528), (2, 4097, 1040), (3, 7168, 1040), (16, 5000, 2064), (8, 8192, 48),
     (1, 16400, 272), (9, 16384, 2064), (20, 16448, 528), (64, 16392, 784),
     (32, 8192, 512), (48, 8193, 96), (17, 8195, 2000), (33, 12000, 1040),
     (24, 32768, 160), (40, 32769, 64), (64, 33000, 272), (18, 40003, 48),
+    (48, 20000, 1040), (30, 20000, 528),
     # prefill kernel
     (65, 256, 128), (200, 300, 400), (256, 256, 256), (300, 772, 1040), (513, 129, 768),
     (600, 1024, 4112),
@@ -275,3 +279,59 @@ def test_prefill_tiles_staged_epilogue(M, N, K, flavour):
         Y = ot.qlinear_asym(dev(Xq), dev(Wq), dev(sW), dev(zW), dev(bp), 8, 8)
         ref = O.epilogue(O.int_gemm_asym(Xq, Wq, zW), sW, bp)
     assert_fp16_close(host(Y), ref)
+
+
+# --------------------------------------------------------------------------
+# Split-K decode: 17-64 tokens with at most 32 output channels per CU, given a
+# workspace, split K over more workgroups and add their int32 partial sums in
+# a second kernel.  The workspace is filled with garbage first (its contents
+# need no initialization); outputs must match the oracle and, bit for bit,
+# the call without a workspace.
+# --------------------------------------------------------------------------
+SPLIT_SHAPES = [(17, 7168, 7168), (32, 5000, 4112), (33, 300, 4112), (48, 8192, 2064),
+                (64, 7168, 28672)]
+
+
+@pytest.mark.parametrize("M,N,K", SPLIT_SHAPES)
+@pytest.mark.parametrize("flavour", ["channel", "token", "asym"])
+def test_decode_split_k(M, N, K, flavour):
+    nbytes = ot.ot_qlinear_workspace_size(M, N, K)
+    case(f"decode split-K {flavour} M={M} N={N} K={K} workspace={nbytes}")
+    assert nbytes > 0, "these sizes take the split path on a 256-CU MI355X"
+    Xq, Wq, sW, bp = _random_qlinear_inputs(M, N, K, 8, 8, 11 * M + N + K)
+    r = np.random.default_rng(M * N)
+    ws = torch.from_numpy(r.integers(0, 256, size=nbytes, dtype=np.uint8)).cuda()
+    args = [dev(Xq), dev(Wq)]
+    if flavour == "channel":
+        call = lambda w: ot.qlinear(*args, dev(sW), dev(bp), 8, 8, want_acc=True, workspace=w)
+        racc = O.int_gemm(Xq, Wq)
+        ref = O.epilogue(racc, sW, bp)
+    elif flavour == "token":
+        sX = r.uniform(0.01, 0.2, size=M).astype(np.float32)
+        call = lambda w: ot.qlinear_per_token(*args, dev(sX), dev(sW), dev(bp), 8, 8,
+                                              want_acc=True, workspace=w)
+        racc = O.int_gemm(Xq, Wq)
+        ref = O.epilogue_per_token(racc, sX, sW, bp)
+    else:
+        zW = r.integers(-128, 128, size=N).astype(np.int32)
+        call = lambda w: ot.qlinear_asym(*args, dev(sW), dev(zW), dev(bp), 8, 8, want_acc=True,
+                                         workspace=w)
+        racc = O.int_gemm_asym(Xq, Wq, zW)
+        ref = O.epilogue(racc, sW, bp)
+    Y, acc = call(ws)
+    assert np.array_equal(host(acc), racc)
+    assert_fp16_close(host(Y), ref)
+    Y0, acc0 = call(None)  # the single-kernel path
+    assert torch.equal(Y, Y0) and torch.equal(acc, acc0)
+    Y1 = call(ws)[0]  # again, on the previous call's leftovers
+    assert torch.equal(Y, Y1)
+
+
+def test_workspace_too_small_is_rejected_by_the_binding():
+    M, N, K = 32, 7168, 7168
+    Xq, Wq, sW, bp = (dev(a) for a in _random_qlinear_inputs(M, N, K, 8, 8, 5))
+    small = torch.empty(ot.ot_qlinear_workspace_size(M, N, K) - 16, dtype=torch.uint8,
+                        device="cuda")
+    case("workspace too small")
+    with pytest.raises(ValueError):
+        ot.qlinear(Xq, Wq, sW, bp, 8, 8, workspace=small)
