@@ -396,8 +396,9 @@ def traffic_record(d, workload):
             raise SystemExit(f"{len(disp)} prefill dispatches is not a whole number of steps")
         for i, (g, v) in enumerate(disp):
             L = wl.layers[i % len(wl.layers)]
-            # the library runs 256 x 256 or 320 (channels) x 256 (tokens) tiles
-            grids = {f"{bn}x256": -(-wl.M // 256) * -(-L.N // bn) * threads for bn in (256, 320)}
+            # the library runs 256 x 256, 320 (channels) x 256 (tokens) or 256 x 128 tiles
+            grids = {f"{bn}x{bm}": -(-wl.M // bm) * -(-L.N // bn) * threads
+                     for bn, bm in ((256, 256), (320, 256), (256, 128))}
             match = [t for t, gg in grids.items() if gg == g]
             if not match:
                 raise SystemExit(f"dispatch {i}: grid {g} fits no tile shape of layer {L.name} "
@@ -415,7 +416,7 @@ def traffic_record(d, workload):
     bench_args = ("--steps 2 --warmup 1 --no-cpu --no-fp16 --no-decode --no-ln --no-mixed "
                   "--no-asym")
     rec = {
-        "kernel": "qgemm_prefill_kernel (256x256 or 320x256 tiles, BK 128, 2 stages)",
+        "kernel": "qgemm_prefill_kernel (256x256, 320x256 or 256x128 tiles, BK 128, 2 stages)",
         "workload": f"{wl.name} ({wl.M} tokens; " + ", ".join(L.name for L in wl.layers) + ")",
         "source_files": [os.path.relpath(p, ROOT) for p in PREFILL_SOURCES],
         "source_sha256": prefill_source_digest(),

@@ -428,36 +428,54 @@ using namespace detail;
 // passes over the CUs, each as long as one tile.  A tile's time is
 // proportional to its products (the matrix cores run power-limited, so the
 // wider tile is no cheaper per product) over K plus its epilogue, which
-// costs about as much as 820 more K steps (measured on MI355X); the wider
-// tile carries a 2 % penalty so that ties keep the 256 x 256 tile.
+// costs about as much as 820 more K steps (measured on MI355X).  Penalties:
+// 2 % for the wider tile, so that ties keep 256 x 256; 1.5 for the shorter
+// tile, which stages 1.5 times the operand bytes per product.
 static double prefill_cost(int64_t M, int64_t N, int64_t K, int bn, int bm, int cus) {
   const int64_t tiles = ((M + bm - 1) / bm) * ((N + bn - 1) / bn);
   const int64_t passes = (tiles + cus - 1) / cus;
-  const double penalty = bn == 320 ? 1.02 : 1.0;
+  const double penalty = bn == 320 ? 1.02 : bm == 128 ? 1.5 : 1.0;
   return (double)passes * bn * bm * ((double)K + 820.0) * penalty;
 }
 
-static bool prefill_uses_wide_tile(int64_t M, int64_t N, int64_t K) {
+// Three tile shapes, each one workgroup of 8 waves per CU with a 2-stage
+// ring of BK = 128:
+//   256 (channels) x 256 (tokens), waves 4 x 2 of 64 x 128 (128 KiB of LDS);
+//   320 x 256, waves 2 x 4 of 160 x 64 (144 KiB): lets layers whose tile
+//     count leaves the last pass over the CUs mostly empty fill whole passes
+//     (4096 tokens by 5120 or 15360 channels: 256 and 768 tiles against 320
+//     and 960 of 256 x 256);
+//   256 x 128, waves 4 x 2 of 64 x 64 (96 KiB): for launches that fill less
+//     than one pass with 256 x 256 (2048 tokens by 4096 channels: 256 tiles
+//     against 128).
+// The cheapest by prefill_cost runs; all give identical results.
+enum class PrefillTile { k256x256, k320x256, k256x128 };
+
+static PrefillTile prefill_tile(int64_t M, int64_t N, int64_t K) {
   const int cus = device_cus();
-  return prefill_cost(M, N, K, 320, 256, cus) < prefill_cost(M, N, K, 256, 256, cus);
+  const double c0 = prefill_cost(M, N, K, 256, 256, cus);
+  const double c1 = prefill_cost(M, N, K, 320, 256, cus);
+  const double c2 = prefill_cost(M, N, K, 256, 128, cus);
+  if (c1 < c0 && c1 <= c2) return PrefillTile::k320x256;
+  if (c2 < c0) return PrefillTile::k256x128;
+  return PrefillTile::k256x256;
 }
 
-// Two tile shapes, both one workgroup of 8 waves per CU with a 2-stage ring
-// of BK = 128: 256 (channels) x 256 (tokens), waves 4 x 2 (128 KiB of LDS),
-// and 320 x 256, waves 2 x 4 (144 KiB).  The wider tile lets layers whose
-// tile count leaves the last pass over the CUs mostly empty fill whole
-// passes instead (4096 tokens by 5120 or 15360 channels: 256 and 768 tiles
-// of 320 x 256 against 320 and 960 of 256 x 256).  The cheaper one by
-// prefill_cost runs; both give identical results.
 hipError_t launch_qgemm_prefill(const int8_t *Xq, const int8_t *Wq, const float *sX,
                                 const int32_t *zW, const float *sW, const float *bprime,
                                 int64_t M, int64_t N, int64_t K, uint16_t *Y, int32_t *acc_out,
                                 hipStream_t st) {
-  if (prefill_uses_wide_tile(M, N, K))
-    return launch_prefill<320, 256, 128, 2, 4, 2>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y,
-                                                  acc_out, st);
-  return launch_prefill<256, 256, 128, 4, 2, 2>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out,
-                                                st);
+  switch (prefill_tile(M, N, K)) {
+    case PrefillTile::k320x256:
+      return launch_prefill<320, 256, 128, 2, 4, 2>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y,
+                                                    acc_out, st);
+    case PrefillTile::k256x128:
+      return launch_prefill<256, 128, 128, 4, 2, 2>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y,
+                                                    acc_out, st);
+    default:
+      return launch_prefill<256, 256, 128, 4, 2, 2>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y,
+                                                    acc_out, st);
+  }
 }
 
 }  // namespace ot

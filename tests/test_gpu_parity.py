@@ -252,12 +252,14 @@ def test_pipeline_opt125m(a_bits, w_bits):
 
 # --------------------------------------------------------------------------
 # Prefill tile shapes and the LDS-staged epilogue (Y only, no acc_out): the
-# library runs 256 x 256 tiles, or 320 (channels) x 256 (tokens) tiles when
-# they need fewer passes over the compute units.  On a 256-CU MI355X the
-# first shape below takes the 320-wide tile (256 tiles against 320 of
-# 256 x 256), the second the 256-wide one; both have ragged M, N and K.
+# library runs 256 x 256, 320 (channels) x 256 (tokens) or 256 x 128 tiles,
+# whichever fills the compute units best.  On a 256-CU MI355X the shapes
+# below take, in order, the 320 x 256 tile (256 tiles against 320 of
+# 256 x 256), the 256 x 128 tile (less than one pass either way) and the
+# 256 x 256 tile (160 tiles, against two passes of 256 x 128); all have
+# ragged M, N and K.
 # --------------------------------------------------------------------------
-PREFILL_TILE_SHAPES = [(500, 40860, 272), (300, 1000, 1040)]
+PREFILL_TILE_SHAPES = [(500, 40860, 272), (300, 1000, 1040), (2000, 5000, 272)]
 
 
 @pytest.mark.parametrize("M,N,K", PREFILL_TILE_SHAPES)
