@@ -16,7 +16,7 @@ namespace ot {
 namespace detail {
 
 constexpr int kWavesPerBlock = 4;
-constexpr int kRowsPerWave = 8;
+constexpr int kRowsPerWave = 4;  // measured best of 1..16 on 4096 x 5120, 4096 x 20480, 8192 x 9216
 
 __device__ inline uint32_t pack4(int a, int b, int c, int d) {
   return (uint32_t)(a & 0xff) | ((uint32_t)(b & 0xff) << 8) | ((uint32_t)(c & 0xff) << 16) |
