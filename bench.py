@@ -61,6 +61,12 @@ def parse():
     p.add_argument("--quality", action="store_true",
                    help="only run the symmetrization ablation / bit-width sweep of output error "
                         "against float64 (one JSON line)")
+    p.add_argument("--decode-probe", action="store_true",
+                   help="only run each decode-regime linear once per token count (for counter runs)")
+    p.add_argument("--counter-summary", metavar="DIR",
+                   help="host only: print the markdown summary of the counter runs under DIR "
+                        "(mfma/ over the prefill step, dram/ over --decode-probe, dram_copy/ over "
+                        "--copy-probe)")
     p.add_argument("--traffic-record", metavar="DIR",
                    help="host only: write the prefill GEMM's HBM traffic record from the "
                         "rocprofv3 counter runs under DIR (fetch/, write/, copy_fetch/, copy_write/)")
@@ -438,6 +444,98 @@ def traffic_record(d, workload):
                                           "copy_factor_fetch", "copy_factor_write")}))
 
 
+def decode_probe(torch, ot, synth, wl, pool):
+    """Each decode-regime linear once per token count, in a fixed order
+    (M ascending, then qkv, out, fc1, fc2), as the bench runs it (workspace
+    where the library uses one); for counter runs."""
+    layers = prepare(wl, max(wl.decode_M), torch, ot, synth, pool)
+    plan = []
+    for M in wl.decode_M:
+        for L in layers:
+            xq = ot.quantize_act(L["X"][:M].contiguous(), wl.a_bits, L["z"], L["inv_s"])
+            y = torch.empty((M, L["N"]), dtype=torch.float16, device="cuda")
+            plan.append((M, L, xq, y, ot.workspace_for(M, L["N"], L["K"])))
+    torch.cuda.synchronize()
+    for M, L, xq, y, ws in plan:
+        ot.ot_qlinear(xq, L["Wq"], L["sW"], L["bp"], wl.a_bits, wl.w_bits, y, workspace=ws)
+    torch.cuda.synchronize()
+    print(json.dumps({"decode_probe": [[M, L["name"], ws is not None] for M, L, _, _, ws in plan]}))
+
+
+def counter_summary(d, workload, decode_workload):
+    """Markdown summary of three rocprofv3 --pmc runs under d (host only):
+    mfma/ (SQ_INSTS_VALU_MFMA_MOPS_I8, SQ_VALU_MFMA_BUSY_CYCLES,
+    SQ_BUSY_CU_CYCLES, GRBM_GUI_ACTIVE, SQ_LDS_BANK_CONFLICT, SQ_INSTS_LDS
+    over the prefill step), dram/ (TCC_EA0_RDREQ_DRAM_32B,
+    TCC_EA0_WRREQ_WRITE_DRAM_32B over --decode-probe) and dram_copy/ (the
+    same over --copy-probe).  rocprofv3 sums each counter over its hardware
+    instances; GRBM_GUI_ACTIVE is counted once per XCD, so it is divided by
+    the 8 XCDs."""
+    import csv
+    import glob
+    from paper_2406_18832_amd import synth
+
+    def dispatches(sub):
+        rows = []
+        for path in sorted(glob.glob(os.path.join(d, sub, "**", "*counter_collection.csv"),
+                                     recursive=True)):
+            with open(path) as f:
+                rows += list(csv.DictReader(f))
+        by = {}
+        for r in rows:
+            e = by.setdefault(int(r["Dispatch_Id"]), {"name": r["Kernel_Name"],
+                                                      "grid": int(r["Grid_Size"])})
+            e[r["Counter_Name"]] = e.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+        return [by[k] for k in sorted(by)]
+
+    simds, xcds = 1024, 8
+    wl = synth.WORKLOADS[workload]
+    pre = [e for e in dispatches("mfma") if "qgemm_prefill_kernel" in e["name"]]
+    out = ["| Layer | Tile | int8 ops counted (MOPS_I8 x 512) | 2MNK | MFMA busy / (GUI active x 1024 SIMDs) | LDS bank-conflict cycles / LDS instr |",
+           "|---|---|---|---|---|---|"]
+    for i, L in enumerate(wl.layers):
+        es = pre[i::len(wl.layers)]
+        ops = np.mean([e["SQ_INSTS_VALU_MFMA_MOPS_I8"] * 512 for e in es])
+        util = np.mean([e["SQ_VALU_MFMA_BUSY_CYCLES"] / (e["GRBM_GUI_ACTIVE"] / xcds * simds)
+                        for e in es])
+        confl = np.mean([e["SQ_LDS_BANK_CONFLICT"] / max(e["SQ_INSTS_LDS"], 1) for e in es])
+        tile = "?"
+        for bn, bm in ((256, 256), (320, 256), (256, 128)):
+            if es[0]["grid"] == -(-wl.M // bm) * -(-L.N // bn) * 512:
+                tile = f"{bn}x{bm}"
+        out.append(f"| {L.name} | {tile} | {ops:.4g} | {2 * wl.M * L.N * L.K:.4g} | {util:.3f} | "
+                   f"{confl:.3f} |")
+    copy = [e for e in dispatches("dram_copy") if "copyBuffer" in e["name"]]
+    n_copy = 1 << 30
+    big = [e for e in copy if e["TCC_EA0_RDREQ_DRAM_32B"] * 32 > n_copy / 4]
+    rd_f = n_copy / float(np.median([e["TCC_EA0_RDREQ_DRAM_32B"] * 32 for e in big]))
+    wr_f = n_copy / float(np.median([e["TCC_EA0_WRREQ_WRITE_DRAM_32B"] * 32 for e in big]))
+    dwl = synth.WORKLOADS[decode_workload]
+    dec = [e for e in dispatches("dram") if "qgemm_decode" in e["name"] or "decode_reduce" in e["name"]]
+    order = [(M, L) for M in dwl.decode_M for L in dwl.layers]
+    out2 = ["| M | Layer | kernels | DRAM read bytes | DRAM write bytes | algorithmic bytes | read / algorithmic |",
+            "|---|---|---|---|---|---|---|"]
+    i = 0
+    for M, L in order:
+        ks = [dec[i]]
+        i += 1
+        if "split" in ks[0]["name"]:
+            ks.append(dec[i])
+            i += 1
+        rd = sum(e["TCC_EA0_RDREQ_DRAM_32B"] for e in ks) * 32 * rd_f
+        wr = sum(e["TCC_EA0_WRREQ_WRITE_DRAM_32B"] for e in ks) * 32 * wr_f
+        alg = L.K * L.N + M * L.K + 2 * M * L.N + 8 * L.N
+        out2.append(f"| {M} | {L.name} | {len(ks)} | {rd / 1e6:.1f} MB | {wr / 1e6:.2f} MB | "
+                    f"{alg / 1e6:.1f} MB | {rd / alg:.3f} |")
+    if i != len(dec):
+        raise SystemExit(f"{len(dec)} decode dispatches, {i} accounted for")
+    print("\n".join(out))
+    print()
+    print(f"DRAM counter calibration on a 1 GiB copy: read factor {rd_f:.3f}, write factor {wr_f:.3f}")
+    print()
+    print("\n".join(out2))
+
+
 def copy_probe(torch):
     """A plain device copy of exactly 1 GiB (read 1 GiB, write 1 GiB)."""
     n = 1 << 30
@@ -487,6 +585,9 @@ def main():
     if args.traffic_record:
         traffic_record(args.traffic_record, args.workload)
         return
+    if args.counter_summary:
+        counter_summary(args.counter_summary, args.workload, args.decode_workload)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the quantized linear "
               "is single-device here and no multi-GPU path is built.", file=sys.stderr)
@@ -497,6 +598,12 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     if args.copy_probe:
         copy_probe(torch)
+        return
+    if args.decode_probe:
+        ot.lib()
+        pool = cf.ThreadPoolExecutor(max_workers=min(16, os.cpu_count() or 4))
+        decode_probe(torch, ot, synth, synth.WORKLOADS[args.decode_workload], pool)
+        pool.shutdown()
         return
     if args.quality:
         from paper_2406_18832_amd import quality
