@@ -10,11 +10,14 @@
 
 namespace {
 
-// Largest K the kernels' 32-bit in-tile offsets cover (a 256-row tile of
-// K-byte rows must stay below 2^31 bytes).
+// Largest K the kernels' 32-bit in-tile offsets cover (a tile of at most
+// 320 K-byte rows must stay below 2^31 bytes).
 constexpr int64_t kMaxK = int64_t(1) << 22;
 constexpr int64_t kMaxLnK = int64_t(1) << 16;  // LayerNorm width (exact sums, one workgroup per row)
 constexpr int64_t kMaxRows = (int64_t(1) << 31) - 1;
+// Prefill workgroups of the smallest tile (128 tokens by 256 channels): the
+// grid must fit a 32-bit count.
+bool grid_ok(int64_t M, int64_t N) { return (M + 127) / 128 * ((N + 255) / 256) <= kMaxRows; }
 
 bool bits_ok(int bits) { return bits >= 2 && bits <= 8; }
 int qmax(int bits) { return (1 << (bits - 1)) - 1; }
@@ -137,7 +140,7 @@ ot_status ot_qlinear(const int8_t *Xq, const int8_t *Wq, const float *sW, const 
   if (!bits_ok(a_bits) || !bits_ok(w_bits) || M < 0 || N < 0 || K < 0) return OT_EINVAL;
   if (N == 0 || K < 16 || K % 16 != 0 || K > kMaxK || M > kMaxRows || N > kMaxRows)
     return OT_ESHAPE;
-  if ((M + 255) / 256 * ((N + 255) / 256) > kMaxRows) return OT_ESHAPE;
+  if (!grid_ok(M, N)) return OT_ESHAPE;
   if (K * qmax(a_bits) * qmax(w_bits) >= (int64_t(1) << 31)) return OT_ERANGE;
   if (M == 0) return OT_OK;
   if (!Xq || !Wq || !sW || !bprime || !Y) return OT_EINVAL;
@@ -181,7 +184,7 @@ ot_status ot_qlinear_per_token(const int8_t *Xq, const int8_t *Wq, const float *
   if (!bits_ok(a_bits) || !bits_ok(w_bits) || M < 0 || N < 0 || K < 0) return OT_EINVAL;
   if (N == 0 || K < 16 || K % 16 != 0 || K > kMaxK || M > kMaxRows || N > kMaxRows)
     return OT_ESHAPE;
-  if ((M + 255) / 256 * ((N + 255) / 256) > kMaxRows) return OT_ESHAPE;
+  if (!grid_ok(M, N)) return OT_ESHAPE;
   if (K * qmax(a_bits) * qmax(w_bits) >= (int64_t(1) << 31)) return OT_ERANGE;
   if (M == 0) return OT_OK;
   if (!Xq || !Wq || !sX || !sW || !bprime || !Y) return OT_EINVAL;
@@ -214,7 +217,7 @@ ot_status ot_qlinear_asym(const int8_t *Xq, const int8_t *Wq, const float *sW, c
   if (!bits_ok(a_bits) || !bits_ok(w_bits) || M < 0 || N < 0 || K < 0) return OT_EINVAL;
   if (N == 0 || K < 16 || K % 16 != 0 || K > kMaxK || M > kMaxRows || N > kMaxRows)
     return OT_ESHAPE;
-  if ((M + 255) / 256 * ((N + 255) / 256) > kMaxRows) return OT_ESHAPE;
+  if (!grid_ok(M, N)) return OT_ESHAPE;
   // |Xq| <= qa against stored codes and zero points of magnitude <= 2^(w_bits-1):
   // every partial sum stays below K qa 2^w_bits
   if (K * qmax(a_bits) * (int64_t(1) << w_bits) >= (int64_t(1) << 31)) return OT_ERANGE;

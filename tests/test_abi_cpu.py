@@ -67,6 +67,7 @@ def _qlinear(M, N, K, a_bits=8, w_bits=8):
     ((4, 0, 32, 8, 8), ot.OT_ESHAPE),      # N = 0
     ((4, 8, 133152, 8, 8), ot.OT_ERANGE),  # K * 127 * 127 >= 2^31
     ((4, 8, 2234640, 6, 6), ot.OT_ERANGE),  # K * 31 * 31 >= 2^31
+    ((1 << 30, 1 << 21, 32, 8, 8), ot.OT_ESHAPE),  # more prefill tiles than a 32-bit grid
     ((0, 8, 32, 8, 8), ot.OT_OK),          # M = 0 is a no-op
     ((4, 8, 32, 8, 8), ot.OT_EINVAL),      # null pointers with work to do
 ])
