@@ -392,10 +392,10 @@ hipError_t launch_qgemm_decode(const int8_t *Xq, const int8_t *Wq, const float *
   // with 128-byte slices run six to a CU.  Below 16 rows per CU, 16-row tiles
   // split over 4 K groups.
   // For 17-64 tokens a workgroup of 8 waves fills most of a CU's LDS, so one
-  // runs per CU: the tile height is the smallest of 32/64/128 rows whose grid
-  // fits in one pass over the CUs (taller tiles re-read the token tile less,
-  // shorter ones use more CUs); past 128 rows per CU, 64-row tiles keep the
-  // last pass's tail short.
+  // runs per CU: the tile height is the smallest of 32/64/96/128 rows whose
+  // grid fits in one pass over the CUs (taller tiles re-read the token tile
+  // less, shorter ones use more CUs); past 128 rows per CU, 64-row tiles keep
+  // the last pass's tail short.
   const int64_t cus = device_cus();
   int per = 0;
   const int sp = workspace ? decode_splits(M, N, K, cus, &per) : 1;
@@ -415,14 +415,20 @@ hipError_t launch_qgemm_decode(const int8_t *Xq, const int8_t *Wq, const float *
       return launch_decode<1, 2, 4, 1, 512, 4>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, st);
     return launch_decode<1, 2, 1, 1, 128, 4>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, st);
   }
-  const int rows = N <= 32 * cus ? 32 : N <= 64 * cus ? 64 : N <= 128 * cus ? 128 : 64;
+  const int rows = N <= 32 * cus    ? 32
+                   : N <= 64 * cus  ? 64
+                   : N <= 96 * cus  ? 96
+                   : N <= 128 * cus ? 128
+                                    : 64;
   if (M <= 32) {
     if (rows == 32) return launch_decode<2, 2, 4, 1, 256, 4>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, st);
     if (rows == 64) return launch_decode<2, 4, 2, 1, 256, 3>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, st);
+    if (rows == 96) return launch_decode<2, 2, 4, 3, 256, 3>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, st);
     return launch_decode<2, 8, 1, 1, 256, 3>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, st);
   }
   if (rows == 32) return launch_decode<4, 2, 4, 1, 256, 4>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, st);
   if (rows == 64) return launch_decode<4, 4, 2, 1, 256, 3>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, st);
+  if (rows == 96) return launch_decode<4, 2, 4, 3, 256, 3>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, st);
   return launch_decode<4, 8, 1, 1, 256, 3>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, st);
 }
 

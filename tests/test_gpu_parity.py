@@ -161,13 +161,15 @@ QL_SHAPES = [
     # decode kernel, every tile for up to 16 tokens (16-row tiles up to
     # N = 4096, 32-row tiles with 512-byte K slices up to 8192, 32-row tiles
     # with 128-byte slices beyond) and every tile height for 17-64 tokens (32
-    # rows up to N = 8192, 64 rows up to 16384, 128 rows up to 32768, 64 rows
-    # beyond), on both sides of each boundary, with ragged N and K tails
+    # rows up to N = 8192, 64 rows up to 16384, 96 rows up to 24576, 128 rows
+    # up to 32768, 64 rows beyond), on both sides of each boundary, with
+    # ragged N and K tails
     (1, 4096, 528), (2, 4097, 1040), (3, 7168, 1040), (16, 5000, 2064), (8, 8192, 48),
     (1, 16400, 272), (9, 16384, 2064), (20, 16448, 528), (64, 16392, 784),
     (32, 8192, 512), (48, 8193, 96), (17, 8195, 2000), (33, 12000, 1040),
     (24, 32768, 160), (40, 32769, 64), (64, 33000, 272), (18, 40003, 48),
-    (48, 20000, 1040), (30, 20000, 528),
+    (48, 20000, 1040), (30, 20000, 528), (64, 24576, 272), (17, 24577, 1040),
+    (40, 30000, 1040),
     # prefill kernel
     (65, 256, 128), (200, 300, 400), (256, 256, 256), (300, 772, 1040), (513, 129, 768),
     (600, 1024, 4112),
