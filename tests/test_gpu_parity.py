@@ -339,3 +339,45 @@ def test_workspace_too_small_is_rejected_by_the_binding():
     case("workspace too small")
     with pytest.raises(ValueError):
         ot.qlinear(Xq, Wq, sW, bp, 8, 8, workspace=small)
+
+
+# --------------------------------------------------------------------------
+# HIP graph replay: a prefill call, a decode call and a split-K decode call
+# (workspace) captured in one graph, replayed several times with eager work
+# and synchronizations in between; every replay must reproduce the eager
+# outputs bit for bit (the kernels clear nothing with memset nodes and keep
+# no state between calls).
+# --------------------------------------------------------------------------
+def test_graph_replay_matches_eager():
+    shapes = [(300, 772, 1040), (8, 7168, 2064), (48, 7168, 2064)]
+    calls = []
+    for i, (M, N, K) in enumerate(shapes):
+        Xq, Wq, sW, bp = (dev(a) for a in _random_qlinear_inputs(M, N, K, 8, 8, 100 + i))
+        Y = torch.empty((M, N), dtype=torch.float16, device="cuda")
+        calls.append((Xq, Wq, sW, bp, Y, ot.workspace_for(M, N, K)))
+    assert calls[2][5] is not None, "the last shape takes the split-K path"
+    case("graph replay of prefill, decode and split-K decode")
+
+    def run():
+        for Xq, Wq, sW, bp, Y, ws in calls:
+            ot.ot_qlinear(Xq, Wq, sW, bp, 8, 8, Y, workspace=ws)
+    run()
+    torch.cuda.synchronize()
+    ref = [c[4].clone() for c in calls]
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(g, stream=s):
+            run()
+    torch.cuda.current_stream().wait_stream(s)
+    other = torch.randn(1 << 20, device="cuda")
+    for rep in range(4):
+        for c in calls:
+            c[4].zero_()
+        other.mul_(1.0001)  # eager work between replays
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for c, r in zip(calls, ref):
+            assert torch.equal(c[4], r), f"replay {rep} differs from the eager outputs"
