@@ -12,7 +12,8 @@ Printed: one JSON line.  `value` is int8 TOPS over the whole step (GEMM ops
 `roofline` covers the dominant kernel (the prefill GEMM) with its duration
 measured by HIP events around each launch inside the timed region; the
 decode regime (OPT-30B shapes, M in {1, 8, 32, 64}) is reported under
-`decode` in GB/s against HBM; `mixed_block` times the paper's own split
+`decode` in GB/s against HBM, on the weights as folded ([N x K]) and on
+packed weights (ot_pack_weights, ot_qlinear_packed); `mixed_block` times the paper's own split
 (per-channel qkv/fc1, per-token out/fc2); `asym_weights` the main step with
 asymmetric ("Int8") weights; `ln_quantize` times the LayerNorm fused with
 symmetrization and quantization (qkv and fc1 inputs) against torch's
@@ -246,6 +247,7 @@ def decode_report(torch, ot, synth, wl, pool, iters, with_fp16):
     layers = prepare(wl, Mmax, torch, ot, synth, pool)
     copies = [layers, [dict(L, Wq=L["Wq"].clone(), sW=L["sW"].clone(), bp=L["bp"].clone())
                        for L in layers]]
+    packed = [[ot.pack_weights(L["Wq"]) for L in c] for c in copies]
     out = {}
     for M in wl.decode_M:
         xq = [ot.quantize_act(L["X"][:M].contiguous(), wl.a_bits, L["z"], L["inv_s"])
@@ -305,6 +307,35 @@ def decode_report(torch, ot, synth, wl, pool, iters, with_fp16):
         rec["graph_GBps"] = nbytes / (gmed * 1e-3) / 1e9
         rec["graph_frac_of_hbm_peak"] = rec["graph_GBps"] / PEAK_HBM_GBS
         del graphs
+        # the same stack on packed weights (ot_pack_weights, untimed, like the
+        # fold), checked bit for bit against the standard layout's outputs
+        yp = [torch.empty_like(y) for y in ys]
+        itp = [0]
+
+        def stack_packed():
+            c = packed[itp[0] & 1]
+            itp[0] += 1
+            for i, L in enumerate(layers):
+                ot.ot_qlinear_packed(xq[i], c[i], L["N"], L["sW"], L["bp"], wl.a_bits,
+                                     wl.w_bits, yp[i], workspace=wsl[i])
+
+        def run_packed():
+            for _ in range(DECODE_RUN):
+                stack_packed()
+        for c in copies:  # one eager stack per copy on the standard layout, for the check
+            for i, L in enumerate(c):
+                ot.ot_qlinear(xq[i], L["Wq"], L["sW"], L["bp"], wl.a_bits, wl.w_bits, ys[i],
+                              workspace=wsl[i])
+        stack_packed()
+        stack_packed()
+        torch.cuda.synchronize()
+        assert all(torch.equal(a, b) for a, b in zip(yp, ys)), "packed outputs differ"
+        pmed, pp10, pp90 = (t / DECODE_RUN for t in median_ms(torch, run_packed, iters))
+        rec["packed_us_per_stack"] = pmed * 1e3
+        rec["packed_p10_us"], rec["packed_p90_us"] = pp10 * 1e3, pp90 * 1e3
+        rec["packed_GBps"] = nbytes / (pmed * 1e-3) / 1e9
+        rec["packed_frac_of_hbm_peak"] = rec["packed_GBps"] / PEAK_HBM_GBS
+        rec["packed_tokens_per_s"] = M / (pmed * 1e-3)
         if with_fp16:
             import torch.nn.functional as F
             w16 = [[L["W16"] for L in layers], [L["W16"].clone() for L in layers]]
@@ -323,7 +354,8 @@ def decode_report(torch, ot, synth, wl, pool, iters, with_fp16):
             del w16
         out[str(M)] = rec
         log(f"decode M={M}: {med * 1e3:.1f} us/stack, {gbs:.0f} GB/s; graph "
-            f"{gmed * 1e3:.1f} us, {rec['graph_GBps']:.0f} GB/s")
+            f"{gmed * 1e3:.1f} us, {rec['graph_GBps']:.0f} GB/s; packed weights "
+            f"{pmed * 1e3:.1f} us, {rec['packed_GBps']:.0f} GB/s")
     return out
 
 

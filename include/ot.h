@@ -286,10 +286,39 @@ ot_status ot_qlinear_per_token(const int8_t *Xq, const int8_t *Wq,
                                int64_t K, int a_bits, int w_bits, uint16_t *Y,
                                int32_t *acc_out, void *workspace, void *stream);
 
-/* Bytes of optional scratch that ot_qlinear, ot_qlinear_per_token and
- * ot_qlinear_asym can use for these sizes on the current device (0 if none;
- * also 0 for sizes the calls reject).  Synchronous, no device work. */
+/* Bytes of optional scratch that ot_qlinear, ot_qlinear_per_token,
+ * ot_qlinear_asym and ot_qlinear_packed can use for these sizes on the
+ * current device (0 if none; also 0 for sizes the calls reject).
+ * Synchronous, no device work. */
 size_t ot_qlinear_workspace_size(int64_t M, int64_t N, int64_t K);
+
+/*
+ * Packed weights for decode.  The folded codes (Eq. (f) right-hand side,
+ * fixed offline like the fold itself, Sec. 3.2) re-laid so that the
+ * weight-streaming kernel reads them as contiguous runs: 1 KiB micro-tiles
+ * of 16 output channels by 64 input channels,
+ *   Wp[g][s][l][b] = Wq[16 g + (l mod 16)][64 s + 16 (l / 16) + b]
+ * for g < ceil(N/16), s < ceil(K/64), lane l < 64, byte b < 16, and 0 where
+ * the row is >= N or the column >= K (the lane order of the A operand of
+ * the 16x16x64 int8 matrix instruction).  The codes are unchanged, so
+ * ot_qlinear_packed gives ot_qlinear's results bit for bit.
+ *
+ * ot_packed_weights_size -- bytes of Wp: ceil(N/16) ceil(K/64) 1024 (0 for
+ *   sizes ot_pack_weights rejects).  No device work.
+ * ot_pack_weights -- Wq [N x K] int8 (device) -> Wp (device, 16-byte
+ *   aligned, ot_packed_weights_size bytes).  N >= 1, K >= 16, K % 16 == 0.
+ *   Asynchronous on stream.
+ * ot_qlinear_packed -- ot_qlinear for M <= 64 tokens (OT_ESHAPE beyond)
+ *   with Wp from ot_pack_weights for the same N and K; the other arguments,
+ *   the workspace and the results as for ot_qlinear.
+ */
+size_t ot_packed_weights_size(int64_t N, int64_t K);
+ot_status ot_pack_weights(const int8_t *Wq, int64_t N, int64_t K, int8_t *Wp,
+                          void *stream);
+ot_status ot_qlinear_packed(const int8_t *Xq, const int8_t *Wp, const float *sW,
+                            const float *bprime, int64_t M, int64_t N, int64_t K,
+                            int a_bits, int w_bits, uint16_t *Y,
+                            int32_t *acc_out, void *workspace, void *stream);
 
 #ifdef __cplusplus
 }

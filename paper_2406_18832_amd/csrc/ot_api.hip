@@ -231,6 +231,35 @@ ot_status ot_qlinear_asym(const int8_t *Xq, const int8_t *Wq, const float *sW, c
                                      workspace, static_cast<hipStream_t>(stream)));
 }
 
+size_t ot_packed_weights_size(int64_t N, int64_t K) {
+  if (N <= 0 || K < 16 || K % 16 != 0 || N > kMaxRows || K > kMaxK) return 0;
+  return ot::packed_weights_bytes(N, K);
+}
+
+ot_status ot_pack_weights(const int8_t *Wq, int64_t N, int64_t K, int8_t *Wp, void *stream) {
+  if (N < 0 || K < 0) return OT_EINVAL;
+  if (N == 0 || K < 16 || K % 16 != 0 || K > kMaxK || N > kMaxRows) return OT_ESHAPE;
+  if (!Wq || !Wp || !aligned16(Wq) || !aligned16(Wp)) return OT_EINVAL;
+  return hip_status(ot::launch_pack_weights(Wq, N, K, Wp, static_cast<hipStream_t>(stream)));
+}
+
+ot_status ot_qlinear_packed(const int8_t *Xq, const int8_t *Wp, const float *sW,
+                            const float *bprime, int64_t M, int64_t N, int64_t K, int a_bits,
+                            int w_bits, uint16_t *Y, int32_t *acc_out, void *workspace,
+                            void *stream) {
+  if (!bits_ok(a_bits) || !bits_ok(w_bits) || M < 0 || N < 0 || K < 0) return OT_EINVAL;
+  if (M > 64 || N == 0 || K < 16 || K % 16 != 0 || K > kMaxK || N > kMaxRows) return OT_ESHAPE;
+  if (K * qmax(a_bits) * qmax(w_bits) >= (int64_t(1) << 31)) return OT_ERANGE;
+  if (M == 0) return OT_OK;
+  if (!Xq || !Wp || !sW || !bprime || !Y) return OT_EINVAL;
+  if (!aligned16(Xq) || !aligned16(Wp) || !aligned16(sW) || !aligned16(bprime) || !aligned16(Y) ||
+      (acc_out && !aligned16(acc_out)) || (workspace && !aligned16(workspace)))
+    return OT_EINVAL;
+  return hip_status(ot::launch_qgemm_decode(Xq, Wp, nullptr, nullptr, sW, bprime, M, N, K, Y,
+                                            acc_out, workspace, true,
+                                            static_cast<hipStream_t>(stream)));
+}
+
 size_t ot_qlinear_workspace_size(int64_t M, int64_t N, int64_t K) {
   if (M <= 0 || N <= 0 || K <= 0 || M > kMaxRows || N > kMaxRows || K > kMaxK) return 0;
   return ot::qgemm_workspace_bytes(M, N, K);

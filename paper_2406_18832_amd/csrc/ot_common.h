@@ -53,10 +53,15 @@ hipError_t launch_quantize_act(const uint16_t *x, int64_t M, int64_t K, int qa, 
 hipError_t launch_ln_quantize_act(const uint16_t *h, int64_t M, int64_t K, const uint16_t *gamma,
                                   const uint16_t *beta, float eps, int qa, const float *z,
                                   const float *inv_s, int8_t *Xq, hipStream_t st);
+// packed: Wq holds micro-tiles from launch_pack_weights instead of [N x K].
 hipError_t launch_qgemm_decode(const int8_t *Xq, const int8_t *Wq, const float *sX,
                                const int32_t *zW, const float *sW, const float *bprime,
                                int64_t M, int64_t N, int64_t K, uint16_t *Y, int32_t *acc_out,
-                               void *workspace, hipStream_t st);
+                               void *workspace, bool packed, hipStream_t st);
+// Decode micro-tile layout of the weight codes (bytes; the packing).
+size_t packed_weights_bytes(int64_t N, int64_t K);
+hipError_t launch_pack_weights(const int8_t *Wq, int64_t N, int64_t K, int8_t *Wp,
+                               hipStream_t st);
 // Scratch bytes the decode kernels use for split-K partial sums (0: none).
 size_t qgemm_decode_workspace_bytes(int64_t M, int64_t N, int64_t K);
 hipError_t launch_qgemm_prefill(const int8_t *Xq, const int8_t *Wq, const float *sX,

@@ -46,6 +46,16 @@ struct DecodeCfg {
 // cache-policy operand of a buffer load on gfx950: non-temporal
 constexpr int kNonTemporal = 2;
 
+// Packed weights (PACKED): Wq re-laid as 1 KiB micro-tiles of 16 rows by 64
+// K bytes, [ceil(N/16)][ceil(K/64)][64 lanes][16 bytes], each in the lane
+// order of the A operand of v_mfma_i32_16x16x64_i8 (lane l: row l mod 16,
+// bytes 16 (l / 16) .. +15 of the 64), zeros past N and K.  A stage then
+// reads one contiguous run of 16 BKD bytes per 16-row group (instead of BKD
+// bytes from each of its rows, K bytes apart), which streams from HBM
+// faster, and a wave's fragment is lane l's 16 bytes at 16 l, free of bank
+// conflicts without a swizzle.
+constexpr int kMicroTile = 1024;
+
 template <int kChunks>
 __device__ __forceinline__ int swz_rows(int r) {
   if constexpr (kChunks == 8) return (r & 7) ^ ((r >> 3) & 1);
@@ -57,7 +67,7 @@ __device__ __forceinline__ int swz_rows(int r) {
 // part[y][m][n] (and, for asymmetric weights, the tokens' partial code sums
 // to part_rs[y][m] from the first row tile); decode_reduce_kernel adds the
 // runs and applies the epilogue.
-template <int MB, int NR, int NK, int RBW, int BKD, int S, int EPI, bool SPLIT>
+template <int MB, int NR, int NK, int RBW, int BKD, int S, int EPI, bool SPLIT, bool PACKED>
 __device__ __forceinline__ void decode_body(
     int8_t *smem, const int8_t *__restrict__ Xq, const int8_t *__restrict__ Wq,
     const float *__restrict__ sX, const int32_t *__restrict__ zW, const float *__restrict__ sW,
@@ -69,23 +79,41 @@ __device__ __forceinline__ void decode_body(
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int rg = wave % NR, kg = wave / NR;
   const int nwg0 = blockIdx.x * C::kWRows;  // first weight row of the workgroup
-  const int rows_w = min(C::kWRows, N - nwg0);
-  const __amdgpu_buffer_rsrc_t rw = make_rsrc(Wq + (int64_t)nwg0 * K, (uint32_t)(rows_w * K));
+  constexpr int kMT = BKD / 64;              // micro-tiles per row group and stage (PACKED)
+  const int KS = (K + 63) / 64;              // micro-tiles per row group (PACKED)
+  __amdgpu_buffer_rsrc_t rw;
+  if constexpr (PACKED) {
+    const int groups_w = min(C::kWRows / 16, (N + 15) / 16 - nwg0 / 16);
+    rw = make_rsrc(Wq + (int64_t)(nwg0 / 16) * KS * kMicroTile,
+                   (uint32_t)groups_w * (uint32_t)KS * kMicroTile);
+  } else {
+    const int rows_w = min(C::kWRows, N - nwg0);
+    rw = make_rsrc(Wq + (int64_t)nwg0 * K, (uint32_t)(rows_w * K));
+  }
   const __amdgpu_buffer_rsrc_t rx = make_rsrc(Xq, (uint32_t)(M * K));
   const int r16 = lane & 15, c4 = lane >> 4;
 
   // this wave's j-th load of a stage fills 1 KiB block q = wave*kLoads + j:
   // stage rows q*kRowsPerLoad.. (tokens below kTokRows, then weights)
+  // (PACKED weight blocks: 1 KiB block qw = q - token blocks is micro-tile
+  // qw mod kMT of row group qw / kMT; gck then holds that micro-tile index)
   uint32_t goff[C::kLoads];
   int gck[C::kLoads];
+  constexpr int kTokBlocks = C::kTokRows / C::kRowsPerLoad;
 #pragma unroll
   for (int j = 0; j < C::kLoads; ++j) {
     const int q = wave * C::kLoads + j;
-    const int row = q * C::kRowsPerLoad + lane / C::kChunks;
-    const int ch = (lane % C::kChunks) ^ swz_rows<C::kChunks>(row);
-    gck[j] = ch * 16;
-    const int grow = row < C::kTokRows ? row : row - C::kTokRows;
-    goff[j] = (uint32_t)(grow * K + ch * 16);
+    if (PACKED && q >= kTokBlocks) {
+      const int qw = q - kTokBlocks;
+      gck[j] = qw % kMT;
+      goff[j] = (uint32_t)(((qw / kMT) * KS + qw % kMT) * kMicroTile + lane * 16);
+    } else {
+      const int row = q * C::kRowsPerLoad + lane / C::kChunks;
+      const int ch = (lane % C::kChunks) ^ swz_rows<C::kChunks>(row);
+      gck[j] = ch * 16;
+      const int grow = row < C::kTokRows ? row : row - C::kTokRows;
+      goff[j] = (uint32_t)(grow * K + ch * 16);
+    }
   }
   // stages [st0, st0 + nst) of K; a split never starts past the last stage
   int st0 = 0, nst = (K + BKD - 1) / BKD;
@@ -99,7 +127,13 @@ __device__ __forceinline__ void decode_body(
 #pragma unroll
     for (int j = 0; j < C::kLoads; ++j) {
       const int q = wave * C::kLoads + j;  // wave-uniform
-      const uint32_t off = (goff[j] + (uint32_t)k0) | ((uint32_t)(k0 + gck[j] >= K) << 31);
+      uint32_t off;
+      if (PACKED && q >= kTokBlocks) {
+        const int mt = (st0 + st) * kMT;  // first micro-tile of the stage
+        off = (goff[j] + (uint32_t)mt * kMicroTile) | ((uint32_t)(mt + gck[j] >= KS) << 31);
+      } else {
+        off = (goff[j] + (uint32_t)k0) | ((uint32_t)(k0 + gck[j] >= K) << 31);
+      }
       // weights are read once: non-temporal ("nt") keeps them from evicting
       // the token rows, which every workgroup re-reads, from the caches
       if (q * C::kRowsPerLoad < C::kTokRows)
@@ -118,8 +152,13 @@ __device__ __forceinline__ void decode_body(
     const int c = 4 * (kg * C::kSteps + t) + c4;
 #pragma unroll
     for (int i = 0; i < RBW; ++i) {
-      const int row = C::kTokRows + (rg * RBW + i) * 16 + r16;
-      fragw[t][i] = row * BKD + 16 * (c ^ swz_rows<C::kChunks>(row));
+      if constexpr (PACKED) {
+        fragw[t][i] = C::kTokRows * BKD +
+                      ((rg * RBW + i) * kMT + kg * C::kSteps + t) * kMicroTile + lane * 16;
+      } else {
+        const int row = C::kTokRows + (rg * RBW + i) * 16 + r16;
+        fragw[t][i] = row * BKD + 16 * (c ^ swz_rows<C::kChunks>(row));
+      }
     }
 #pragma unroll
     for (int j = 0; j < MB; ++j) {
@@ -248,25 +287,25 @@ __device__ __forceinline__ void decode_body(
   }
 }
 
-template <int MB, int NR, int NK, int RBW, int BKD, int S, int EPI>
+template <int MB, int NR, int NK, int RBW, int BKD, int S, int EPI, bool PACKED>
 __global__ __launch_bounds__(64 * NR * NK) void qgemm_decode_kernel(
     const int8_t *__restrict__ Xq, const int8_t *__restrict__ Wq, const float *__restrict__ sX,
     const int32_t *__restrict__ zW, const float *__restrict__ sW, const float *__restrict__ bp,
     int M, int N, int K, uint16_t *__restrict__ Y, int32_t *__restrict__ acc_out) {
   __shared__ __attribute__((aligned(1024)))
   int8_t smem[S * DecodeCfg<MB, NR, NK, RBW, BKD, S>::kStage];
-  decode_body<MB, NR, NK, RBW, BKD, S, EPI, false>(smem, Xq, Wq, sX, zW, sW, bp, M, N, K, Y,
-                                                   acc_out, nullptr, nullptr, 0);
+  decode_body<MB, NR, NK, RBW, BKD, S, EPI, false, PACKED>(smem, Xq, Wq, sX, zW, sW, bp, M, N, K,
+                                                           Y, acc_out, nullptr, nullptr, 0);
 }
 
 // Split-K partial sums (ROWSUM: also the token code sums of asymmetric weights).
-template <int MB, int NR, int NK, int RBW, int BKD, int S, bool ROWSUM>
+template <int MB, int NR, int NK, int RBW, int BKD, int S, bool ROWSUM, bool PACKED>
 __global__ __launch_bounds__(64 * NR * NK) void qgemm_decode_split_kernel(
     const int8_t *__restrict__ Xq, const int8_t *__restrict__ Wq, int M, int N, int K,
     int32_t *__restrict__ part, int32_t *__restrict__ part_rs, int per) {
   __shared__ __attribute__((aligned(1024)))
   int8_t smem[S * DecodeCfg<MB, NR, NK, RBW, BKD, S>::kStage];
-  decode_body<MB, NR, NK, RBW, BKD, S, ROWSUM ? kEpiAsym : kEpiChannel, true>(
+  decode_body<MB, NR, NK, RBW, BKD, S, ROWSUM ? kEpiAsym : kEpiChannel, true, PACKED>(
       smem, Xq, Wq, nullptr, nullptr, nullptr, nullptr, M, N, K, nullptr, nullptr, part, part_rs,
       per);
 }
@@ -301,7 +340,7 @@ __global__ __launch_bounds__(256) void decode_reduce_kernel(
   store4<EPI>(Y, acc_out, sW, bp, zW, sx, rs, m, n, M, N, a[0], a[1], a[2], a[3]);
 }
 
-template <int MB, int NR, int NK, int RBW, int BKD, int S>
+template <int MB, int NR, int NK, int RBW, int BKD, int S, bool PACKED>
 hipError_t launch_decode_split(const int8_t *Xq, const int8_t *Wq, const float *sX,
                                const int32_t *zW, const float *sW, const float *bp, int64_t M,
                                int64_t N, int64_t K, uint16_t *Y, int32_t *acc_out, int splits,
@@ -310,10 +349,10 @@ hipError_t launch_decode_split(const int8_t *Xq, const int8_t *Wq, const float *
   const dim3 grid((unsigned)((N + rows - 1) / rows), (unsigned)splits);
   const dim3 block(64 * NR * NK);
   if (zW)
-    qgemm_decode_split_kernel<MB, NR, NK, RBW, BKD, S, true><<<grid, block, 0, st>>>(
+    qgemm_decode_split_kernel<MB, NR, NK, RBW, BKD, S, true, PACKED><<<grid, block, 0, st>>>(
         Xq, Wq, (int)M, (int)N, (int)K, part, part_rs, per);
   else
-    qgemm_decode_split_kernel<MB, NR, NK, RBW, BKD, S, false><<<grid, block, 0, st>>>(
+    qgemm_decode_split_kernel<MB, NR, NK, RBW, BKD, S, false, PACKED><<<grid, block, 0, st>>>(
         Xq, Wq, (int)M, (int)N, (int)K, part, part_rs, per);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
@@ -332,23 +371,52 @@ hipError_t launch_decode_split(const int8_t *Xq, const int8_t *Wq, const float *
 
 // Epilogue by argument: sX != nullptr per-token scales sX [M]; zW != nullptr
 // asymmetric weight zero points zW [N]; neither: per-channel.
-template <int MB, int NR, int NK, int RBW, int BKD, int S>
-hipError_t launch_decode(const int8_t *Xq, const int8_t *Wq, const float *sX, const int32_t *zW,
-                         const float *sW, const float *bp, int64_t M, int64_t N, int64_t K,
-                         uint16_t *Y, int32_t *acc_out, hipStream_t st) {
+template <int MB, int NR, int NK, int RBW, int BKD, int S, bool PACKED>
+hipError_t launch_decode_t(const int8_t *Xq, const int8_t *Wq, const float *sX, const int32_t *zW,
+                           const float *sW, const float *bp, int64_t M, int64_t N, int64_t K,
+                           uint16_t *Y, int32_t *acc_out, hipStream_t st) {
   constexpr int rows = 16 * RBW * NR;
   const unsigned grid = (unsigned)((N + rows - 1) / rows);
   const dim3 block(64 * NR * NK);
   if (sX)
-    qgemm_decode_kernel<MB, NR, NK, RBW, BKD, S, kEpiToken><<<grid, block, 0, st>>>(
+    qgemm_decode_kernel<MB, NR, NK, RBW, BKD, S, kEpiToken, PACKED><<<grid, block, 0, st>>>(
         Xq, Wq, sX, zW, sW, bp, (int)M, (int)N, (int)K, Y, acc_out);
   else if (zW)
-    qgemm_decode_kernel<MB, NR, NK, RBW, BKD, S, kEpiAsym><<<grid, block, 0, st>>>(
+    qgemm_decode_kernel<MB, NR, NK, RBW, BKD, S, kEpiAsym, PACKED><<<grid, block, 0, st>>>(
         Xq, Wq, sX, zW, sW, bp, (int)M, (int)N, (int)K, Y, acc_out);
   else
-    qgemm_decode_kernel<MB, NR, NK, RBW, BKD, S, kEpiChannel><<<grid, block, 0, st>>>(
+    qgemm_decode_kernel<MB, NR, NK, RBW, BKD, S, kEpiChannel, PACKED><<<grid, block, 0, st>>>(
         Xq, Wq, sX, zW, sW, bp, (int)M, (int)N, (int)K, Y, acc_out);
   return hipGetLastError();
+}
+
+// Weight layout by argument: packed micro-tiles or Wq [N x K].
+template <int MB, int NR, int NK, int RBW, int BKD, int S>
+hipError_t launch_decode(const int8_t *Xq, const int8_t *Wq, const float *sX, const int32_t *zW,
+                         const float *sW, const float *bp, int64_t M, int64_t N, int64_t K,
+                         uint16_t *Y, int32_t *acc_out, bool packed, hipStream_t st) {
+  if (packed)
+    return launch_decode_t<MB, NR, NK, RBW, BKD, S, true>(Xq, Wq, sX, zW, sW, bp, M, N, K, Y,
+                                                          acc_out, st);
+  return launch_decode_t<MB, NR, NK, RBW, BKD, S, false>(Xq, Wq, sX, zW, sW, bp, M, N, K, Y,
+                                                         acc_out, st);
+}
+
+// Packs Wq [N x K] into micro-tiles (see PACKED above): thread t writes the
+// 16 bytes of lane t mod 64 of micro-tile t / 64.
+__global__ __launch_bounds__(256) void pack_weights_kernel(const int8_t *__restrict__ Wq,
+                                                           int64_t N, int64_t K, int64_t KS,
+                                                           int64_t chunks,
+                                                           int8_t *__restrict__ Wp) {
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (t >= chunks) return;
+  const int l = (int)(t & 63);
+  const int64_t mt = t >> 6;  // micro-tile: row group mt / KS, K step mt mod KS
+  const int64_t row = (mt / KS) * 16 + (l & 15);
+  const int64_t col = (mt % KS) * 64 + 16 * (l >> 4);
+  uint4 v = make_uint4(0, 0, 0, 0);
+  if (row < N && col < K) v = *reinterpret_cast<const uint4 *>(Wq + row * K + col);
+  reinterpret_cast<uint4 *>(Wp)[t] = v;
 }
 
 }  // namespace detail
@@ -378,10 +446,23 @@ size_t qgemm_decode_workspace_bytes(int64_t M, int64_t N, int64_t K) {
   return sp > 1 ? (size_t)sp * (size_t)M * (size_t)(N + 1) * sizeof(int32_t) : 0;
 }
 
+size_t packed_weights_bytes(int64_t N, int64_t K) {
+  return (size_t)((N + 15) / 16) * (size_t)((K + 63) / 64) * kMicroTile;
+}
+
+hipError_t launch_pack_weights(const int8_t *Wq, int64_t N, int64_t K, int8_t *Wp,
+                               hipStream_t st) {
+  const int64_t KS = (K + 63) / 64;
+  const int64_t chunks = (N + 15) / 16 * KS * 64;
+  pack_weights_kernel<<<(unsigned)((chunks + 255) / 256), 256, 0, st>>>(Wq, N, K, KS, chunks, Wp);
+  return hipGetLastError();
+}
+
+// Wq: the weight codes [N x K], or (packed) their micro-tiles.
 hipError_t launch_qgemm_decode(const int8_t *Xq, const int8_t *Wq, const float *sX,
                                const int32_t *zW, const float *sW, const float *bprime,
                                int64_t M, int64_t N, int64_t K, uint16_t *Y, int32_t *acc_out,
-                               void *workspace, hipStream_t st) {
+                               void *workspace, bool packed, hipStream_t st) {
   // Template arguments
   // <token blocks, row groups, K groups, row blocks per wave, BKD, stages>,
   // chosen from a sweep of every valid configuration on the OPT-30B layers
@@ -403,17 +484,21 @@ hipError_t launch_qgemm_decode(const int8_t *Xq, const int8_t *Wq, const float *
     int32_t *part = static_cast<int32_t *>(workspace);
     int32_t *part_rs = part + (int64_t)sp * M * N;
     if (M <= 32)
-      return launch_decode_split<2, 8, 1, 1, 256, 3>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y,
-                                                     acc_out, sp, per, part, part_rs, st);
-    return launch_decode_split<4, 8, 1, 1, 256, 3>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y,
-                                                   acc_out, sp, per, part, part_rs, st);
+      return packed ? launch_decode_split<2, 8, 1, 1, 256, 3, true>(
+                          Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, sp, per, part, part_rs, st)
+                    : launch_decode_split<2, 8, 1, 1, 256, 3, false>(
+                          Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, sp, per, part, part_rs, st);
+    return packed ? launch_decode_split<4, 8, 1, 1, 256, 3, true>(
+                        Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, sp, per, part, part_rs, st)
+                  : launch_decode_split<4, 8, 1, 1, 256, 3, false>(
+                        Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, sp, per, part, part_rs, st);
   }
   if (M <= 16) {
     if (N <= 16 * cus)
-      return launch_decode<1, 1, 4, 1, 256, 4>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, st);
+      return launch_decode<1, 1, 4, 1, 256, 4>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, packed, st);
     if (N <= 32 * cus)
-      return launch_decode<1, 2, 4, 1, 512, 4>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, st);
-    return launch_decode<1, 2, 1, 1, 128, 4>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, st);
+      return launch_decode<1, 2, 4, 1, 512, 4>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, packed, st);
+    return launch_decode<1, 2, 1, 1, 128, 4>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, packed, st);
   }
   const int rows = N <= 32 * cus    ? 32
                    : N <= 64 * cus  ? 64
@@ -421,15 +506,15 @@ hipError_t launch_qgemm_decode(const int8_t *Xq, const int8_t *Wq, const float *
                    : N <= 128 * cus ? 128
                                     : 64;
   if (M <= 32) {
-    if (rows == 32) return launch_decode<2, 2, 4, 1, 256, 4>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, st);
-    if (rows == 64) return launch_decode<2, 4, 2, 1, 256, 3>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, st);
-    if (rows == 96) return launch_decode<2, 2, 4, 3, 256, 3>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, st);
-    return launch_decode<2, 8, 1, 1, 256, 3>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, st);
+    if (rows == 32) return launch_decode<2, 2, 4, 1, 256, 4>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, packed, st);
+    if (rows == 64) return launch_decode<2, 4, 2, 1, 256, 3>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, packed, st);
+    if (rows == 96) return launch_decode<2, 2, 4, 3, 256, 3>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, packed, st);
+    return launch_decode<2, 8, 1, 1, 256, 3>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, packed, st);
   }
-  if (rows == 32) return launch_decode<4, 2, 4, 1, 256, 4>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, st);
-  if (rows == 64) return launch_decode<4, 4, 2, 1, 256, 3>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, st);
-  if (rows == 96) return launch_decode<4, 2, 4, 3, 256, 3>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, st);
-  return launch_decode<4, 8, 1, 1, 256, 3>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, st);
+  if (rows == 32) return launch_decode<4, 2, 4, 1, 256, 4>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, packed, st);
+  if (rows == 64) return launch_decode<4, 4, 2, 1, 256, 3>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, packed, st);
+  if (rows == 96) return launch_decode<4, 2, 4, 3, 256, 3>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, packed, st);
+  return launch_decode<4, 8, 1, 1, 256, 3>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, packed, st);
 }
 
 }  // namespace ot

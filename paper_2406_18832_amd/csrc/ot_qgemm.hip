@@ -31,7 +31,8 @@ hipError_t launch_qgemm(const int8_t *Xq, const int8_t *Wq, const float *sX, con
                         const float *sW, const float *bprime, int64_t M, int64_t N, int64_t K,
                         uint16_t *Y, int32_t *acc_out, void *workspace, hipStream_t st) {
   if (M <= 64)
-    return launch_qgemm_decode(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, workspace, st);
+    return launch_qgemm_decode(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, workspace, false,
+                               st);
   return launch_qgemm_prefill(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, st);
 }
 

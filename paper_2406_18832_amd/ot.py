@@ -71,6 +71,12 @@ def lib() -> ctypes.CDLL:
         L.ot_qlinear.argtypes = [vp, vp, vp, vp, i64, i64, i64, c_int, c_int, vp, vp, vp, vp]
         L.ot_qlinear_workspace_size.restype = ctypes.c_size_t
         L.ot_qlinear_workspace_size.argtypes = [i64, i64, i64]
+        L.ot_packed_weights_size.restype = ctypes.c_size_t
+        L.ot_packed_weights_size.argtypes = [i64, i64]
+        L.ot_pack_weights.restype = c_int
+        L.ot_pack_weights.argtypes = [vp, i64, i64, vp, vp]
+        L.ot_qlinear_packed.restype = c_int
+        L.ot_qlinear_packed.argtypes = [vp, vp, vp, vp, i64, i64, i64, c_int, c_int, vp, vp, vp, vp]
         _lib = L
     return _lib
 
@@ -196,6 +202,35 @@ def ot_qlinear(Xq, Wq, sW, bprime, a_bits, w_bits, Y, acc_out=None, workspace=No
 
 def ot_qlinear_workspace_size(M: int, N: int, K: int) -> int:
     return int(lib().ot_qlinear_workspace_size(M, N, K))
+
+
+def ot_packed_weights_size(N: int, K: int) -> int:
+    return int(lib().ot_packed_weights_size(N, K))
+
+
+def ot_pack_weights(Wq, Wp, stream=None):
+    """Wq [N, K] int8 -> Wp (ot_packed_weights_size(N, K) bytes, int8), the
+    decode micro-tile layout.  Asynchronous."""
+    N, K = Wq.shape
+    rc = lib().ot_pack_weights(_dev(Wq, torch.int8, "Wq"), N, K,
+                               _dev(Wp, torch.int8, "Wp", (ot_packed_weights_size(N, K),)),
+                               _stream(stream))
+    _check(rc, "ot_pack_weights")
+
+
+def ot_qlinear_packed(Xq, Wp, N, sW, bprime, a_bits, w_bits, Y, acc_out=None, workspace=None,
+                      stream=None):
+    """ot_qlinear for M <= 64 with packed weights Wp (of N output channels)
+    from ot_pack_weights.  Asynchronous."""
+    M, K = Xq.shape
+    rc = lib().ot_qlinear_packed(_dev(Xq, torch.int8, "Xq"),
+                                 _dev(Wp, torch.int8, "Wp", (ot_packed_weights_size(N, K),)),
+                                 _dev(sW, torch.float32, "sW", (N,)),
+                                 _dev(bprime, torch.float32, "bprime", (N,)), M, N, K,
+                                 int(a_bits), int(w_bits), _dev(Y, torch.float16, "Y", (M, N)),
+                                 _dev(acc_out, torch.int32, "acc_out", (M, N)),
+                                 _dev_ws(workspace, M, N, K), _stream(stream))
+    _check(rc, "ot_qlinear_packed")
 
 
 # ---------------------------------------------------------------------------
@@ -357,6 +392,23 @@ def qlinear(Xq, Wq, sW, bprime, a_bits, w_bits, want_acc=False, workspace=None):
     Y = torch.empty((M, N), dtype=torch.float16, device=Xq.device)
     acc = torch.empty((M, N), dtype=torch.int32, device=Xq.device) if want_acc else None
     ot_qlinear(Xq, Wq, sW, bprime, a_bits, w_bits, Y, acc, _ws(workspace, Xq, Wq))
+    return (Y, acc) if want_acc else Y
+
+
+def pack_weights(Wq):
+    N, K = Wq.shape
+    Wp = torch.empty(ot_packed_weights_size(N, K), dtype=torch.int8, device=Wq.device)
+    ot_pack_weights(Wq, Wp)
+    return Wp
+
+
+def qlinear_packed(Xq, Wp, N, sW, bprime, a_bits, w_bits, want_acc=False, workspace=None):
+    M, K = Xq.shape
+    Y = torch.empty((M, N), dtype=torch.float16, device=Xq.device)
+    acc = torch.empty((M, N), dtype=torch.int32, device=Xq.device) if want_acc else None
+    ws = workspace_for(M, N, K, Xq.device) if workspace is True else (
+        None if workspace is None or workspace is False else workspace)
+    ot_qlinear_packed(Xq, Wp, N, sW, bprime, a_bits, w_bits, Y, acc, ws)
     return (Y, acc) if want_acc else Y
 
 

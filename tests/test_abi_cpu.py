@@ -166,3 +166,20 @@ def test_binding_workspace_argument_forms():
     assert ot._ws(t, x, w) is t
     with pytest.raises(ValueError):
         ot._dev_ws(torch.empty(8, dtype=torch.uint8), 2, 4, 16)  # host tensor
+
+
+def test_packed_weights_size_and_argument_checks():
+    sz = ot.ot_packed_weights_size
+    assert sz(16, 64) == 1024 and sz(17, 80) == 2 * 2 * 1024 and sz(7168, 7168) == 448 * 112 * 1024
+    assert sz(0, 64) == 0 and sz(16, 24) == 0 and sz(16, 0) == 0
+    L = ot.lib()
+    assert L.ot_pack_weights(None, 16, 24, None, None) == ot.OT_ESHAPE  # K % 16
+    assert L.ot_pack_weights(None, 16, 64, None, None) == ot.OT_EINVAL      # null pointers
+    q = lambda M, N, K, a=8, w=8: L.ot_qlinear_packed(None, None, None, None, M, N, K, a, w,
+                                                       None, None, None, None)
+    assert q(65, 8, 32) == ot.OT_ESHAPE      # decode only
+    assert q(4, 8, 24) == ot.OT_ESHAPE       # K % 16
+    assert q(4, 8, 133152) == ot.OT_ERANGE   # int32 accumulator bound
+    assert q(0, 8, 32) == ot.OT_OK           # no work
+    assert q(4, 8, 32) == ot.OT_EINVAL       # null pointers
+    assert q(4, 8, 32, 9) == ot.OT_EINVAL    # bits

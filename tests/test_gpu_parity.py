@@ -381,3 +381,54 @@ def test_graph_replay_matches_eager():
         torch.cuda.synchronize()
         for c, r in zip(calls, ref):
             assert torch.equal(c[4], r), f"replay {rep} differs from the eager outputs"
+
+
+# --------------------------------------------------------------------------
+# Packed decode weights: the layout matches its definition (a re-layout of
+# the codes, zero-padded), and ot_qlinear_packed gives ot_qlinear's outputs
+# bit for bit on every decode shape, with and without the split-K workspace.
+# --------------------------------------------------------------------------
+def _pack_reference(Wq):
+    N, K = Wq.shape
+    G, KS = -(-N // 16), -(-K // 64)
+    padded = np.zeros((G * 16, KS * 64), dtype=np.int8)
+    padded[:N, :K] = Wq
+    # [g][r][s][c][b] -> [g][s][c][r][b]: lane = r + 16 c
+    t = padded.reshape(G, 16, KS, 4, 16).transpose(0, 2, 3, 1, 4)
+    return t.reshape(-1)
+
+
+@pytest.mark.parametrize("N,K", [(16, 64), (17, 80), (300, 1040), (7168, 2064)])
+def test_pack_weights_layout(N, K):
+    Wq = np.random.default_rng(N + K).integers(-128, 128, size=(N, K)).astype(np.int8)
+    case(f"pack weights N={N} K={K}")
+    Wp = host(ot.pack_weights(dev(Wq)))
+    assert np.array_equal(Wp, _pack_reference(Wq))
+
+
+PACKED_SHAPES = [s for s in QL_SHAPES if s[0] <= 64]
+
+
+@pytest.mark.parametrize("M,N,K", PACKED_SHAPES)
+def test_qlinear_packed_parity(M, N, K):
+    Xq, Wq, sW, bp = _random_qlinear_inputs(M, N, K, 8, 8, 7 * M + N + 3 * K)
+    case(f"qlinear packed M={M} N={N} K={K}")
+    Wp = ot.pack_weights(dev(Wq))
+    Y, acc = ot.qlinear_packed(dev(Xq), Wp, N, dev(sW), dev(bp), 8, 8, want_acc=True)
+    racc = O.int_gemm(Xq, Wq)
+    assert np.array_equal(host(acc), racc)
+    assert_fp16_close(host(Y), O.epilogue(racc, sW, bp))
+    Y0 = ot.qlinear(dev(Xq), dev(Wq), dev(sW), dev(bp), 8, 8)
+    assert torch.equal(Y, Y0)
+
+
+@pytest.mark.parametrize("M,N,K", SPLIT_SHAPES)
+def test_qlinear_packed_split_k(M, N, K):
+    Xq, Wq, sW, bp = _random_qlinear_inputs(M, N, K, 8, 8, 13 * M + N + K)
+    case(f"qlinear packed split-K M={M} N={N} K={K}")
+    Wp = ot.pack_weights(dev(Wq))
+    Y, acc = ot.qlinear_packed(dev(Xq), Wp, N, dev(sW), dev(bp), 8, 8, want_acc=True,
+                               workspace=True)
+    racc = O.int_gemm(Xq, Wq)
+    assert np.array_equal(host(acc), racc)
+    assert_fp16_close(host(Y), O.epilogue(racc, sW, bp))
