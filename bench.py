@@ -581,6 +581,18 @@ def copy_probe(torch):
     print(json.dumps({"copy_probe_bytes_read": n, "copy_probe_bytes_written": n, "launches": 3}))
 
 
+def hbm_copy_context(torch, iters=10):
+    """A plain 1 GiB device-to-device copy (torch's), for context: bytes read
+    plus written per second."""
+    n = 1 << 30
+    a = torch.empty(n, dtype=torch.uint8, device="cuda")
+    a.fill_(1)
+    b = torch.empty_like(a)
+    med, _, _ = median_ms(torch, lambda: b.copy_(a), iters)
+    del a, b
+    return dict(bytes_read_and_written=2 * n, ms=med, GBps=2 * n / (med * 1e-3) / 1e9)
+
+
 def cpu_baseline(ot_oracle, layers, M, budget_s=10.0):
     """The oracle's quantize + integer GEMM + epilogue on the first R token
     rows of every linear, R doubled until the sample takes `budget_s`."""
@@ -742,6 +754,10 @@ def main():
         result["decode"] = {"workload": dwl.name, "bound": "hbm", "peak_GBps": PEAK_HBM_GBS,
                             "by_M": decode_report(torch, ot, synth, dwl, pool, args.iters,
                                                   not args.no_fp16)}
+        torch.cuda.empty_cache()
+        result["decode"]["hbm_copy_context"] = hbm_copy_context(torch)
+        log(f"plain 1 GiB device copy: {result['decode']['hbm_copy_context']['GBps']:.0f} GB/s "
+            f"(read + write)")
     pool.shutdown()
     print(json.dumps(result), flush=True)
 
