@@ -192,10 +192,12 @@ ot_status ot_ln_quantize_act(const uint16_t *h, int64_t M, int64_t K,
  *   workspace  NULL, or at least ot_qlinear_workspace_size(M, N, K) bytes of
  *           16-byte-aligned device memory the call may use as scratch; with
  *           NULL the call uses no scratch memory.  Results do not depend on
- *           it.  For 17..64 tokens and at most 32 output channels per compute
- *           unit the call then splits K over more workgroups and adds their
- *           int32 partial sums in a second kernel (the sums are exact, so the
- *           outputs are identical).  The contents need no initialization and
+ *           it.  For 17..64 tokens, where the launch plan finds it faster
+ *           (layers with few output channels per compute unit and long K),
+ *           the call then splits K over more workgroups and adds their int32
+ *           partial sums in a second kernel (the sums are exact, so the
+ *           outputs are identical); ot_qlinear_workspace_size returns 0
+ *           where it does not.  The contents need no initialization and
  *           are left unspecified; calls that overlap in time must not share
  *           a workspace.
  *

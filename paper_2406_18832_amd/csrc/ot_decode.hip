@@ -423,27 +423,69 @@ __global__ __launch_bounds__(256) void pack_weights_kernel(const int8_t *__restr
 
 using namespace detail;
 
-// Split K for 17-64 tokens: with at most 32 weight rows per CU the 128-row
-// tiles that keep the token re-reads low leave CUs idle, so each row tile's
-// K is cut into runs of whole 256-byte stages (at least 4 per run, at most
-// 8 runs) that fill the CUs; a second kernel adds the runs' int32 partial
-// sums (splits x M x N, plus splits x M token code sums) and applies the
-// epilogue.  Returns the number of runs, 1 for no split.
-static int decode_splits(int64_t M, int64_t N, int64_t K, int64_t cus, int *per_out) {
-  constexpr int kRows = 128, kBKD = 256;
-  if (M <= 16 || M > 64 || N > 32 * cus) return 1;
-  const int64_t tiles = (N + kRows - 1) / kRows;
-  const int64_t nst = (K + kBKD - 1) / kBKD;
-  int64_t sp = std::min<int64_t>(std::min<int64_t>(cus / tiles, nst / 4), 8);
-  if (sp < 2) return 1;
-  const int64_t per = (nst + sp - 1) / sp;  // stages per run; no run is empty
-  if (per_out) *per_out = (int)per;
-  return (int)((nst + per - 1) / per);
+// Launch plan for 17-64 tokens: the tile height (weight rows per workgroup)
+// and the number of K runs (split K: each run writes int32 partial sums
+// that a second kernel adds up).  Every candidate grid fits one pass over
+// the CUs (one 8-wave workgroup fills most of a CU's LDS); the plan with the
+// least estimated time wins.  The estimate, in microseconds, was fitted to
+// every (tile height, runs) pair measured on MI355X for 13 layer shapes
+// (N = 2048 .. 21504, K = 2048 .. 36864) at 24, 32, 48 and 64 tokens, and
+// keeps the fit's physical reading:
+//   each CU streams its weight rows plus the token rows (L2 hits, counted
+//   half) of its K run at ~40 GB/s;
+//   the whole chip streams the weights from HBM at ~6 TB/s, and weights
+//   plus every tile's token re-read from L2 at ~10 TB/s;
+//   a split adds ~2 us (the reduce launch) plus its runs x M x N int32
+//   partial sums, written and read back at ~2 TB/s.
+// Taller tiles re-read the token tile less (M / rows bytes per weight
+// byte); splits fill CUs that short, wide-K layers would leave idle.
+struct DecodePlan {
+  int rows;  // 32, 64, 96 or 128
+  int runs;  // K runs; 1 = one kernel with the epilogue
+  int per;   // K stages of the tile's BKD bytes per run
+};
+
+constexpr int plan_bkd(int rows) { return rows == 128 ? 128 : 256; }
+
+static double plan_cost(int64_t M, int64_t N, int64_t K, int rows, int runs, int64_t cus) {
+  const double chip = (double)cus / 256.0;  // bandwidths below are for 256 CUs
+  const double kr = (double)K / runs;
+  const double tiles = (double)((N + rows - 1) / rows);
+  const double per_cu = (rows + 0.5 * M) * kr / 40e3;
+  const double hbm = (double)N * K / (6e6 * chip);
+  const double l2 = ((double)N * K + tiles * M * K) / (10e6 * chip);
+  double t = std::max(per_cu, std::max(hbm, l2));
+  if (runs > 1) t += 2.0 + (double)runs * M * N * 8 / (2e6 * chip);
+  return t;
+}
+
+static DecodePlan decode_plan(int64_t M, int64_t N, int64_t K, int64_t cus, bool split) {
+  // past 128 rows per CU no grid fits one pass: 64-row tiles keep the last
+  // pass's tail short
+  DecodePlan best{64, 1, 0};
+  double best_t = 0;
+  for (int rows : {32, 64, 96, 128}) {
+    const int64_t tiles = (N + rows - 1) / rows;
+    if (tiles > cus) continue;
+    const int64_t nst = (K + plan_bkd(rows) - 1) / plan_bkd(rows);
+    for (int runs = 1; runs <= (split ? 8 : 1) && tiles * runs <= cus; ++runs) {
+      if (runs > 1 && (K + 255) / 256 < 4 * runs) break;  // runs of at least 1 KiB of K
+      const int64_t per = (nst + runs - 1) / runs;
+      if ((nst + per - 1) / per != runs) continue;  // no run may be empty
+      const double t = plan_cost(M, N, K, rows, runs, cus);
+      if (best_t == 0 || t < best_t) {
+        best = DecodePlan{rows, runs, (int)per};
+        best_t = t;
+      }
+    }
+  }
+  return best;
 }
 
 size_t qgemm_decode_workspace_bytes(int64_t M, int64_t N, int64_t K) {
-  const int sp = decode_splits(M, N, K, device_cus(), nullptr);
-  return sp > 1 ? (size_t)sp * (size_t)M * (size_t)(N + 1) * sizeof(int32_t) : 0;
+  if (M <= 16 || M > 64) return 0;
+  const DecodePlan p = decode_plan(M, N, K, device_cus(), true);
+  return p.runs > 1 ? (size_t)p.runs * (size_t)M * (size_t)(N + 1) * sizeof(int32_t) : 0;
 }
 
 size_t packed_weights_bytes(int64_t N, int64_t K) {
@@ -465,34 +507,14 @@ hipError_t launch_qgemm_decode(const int8_t *Xq, const int8_t *Wq, const float *
                                void *workspace, bool packed, hipStream_t st) {
   // Template arguments
   // <token blocks, row groups, K groups, row blocks per wave, BKD, stages>,
-  // chosen from a sweep of every valid configuration on the OPT-30B layers
-  // (N = 7168 .. 28672) at 1 .. 64 tokens on MI355X.
+  // chosen from sweeps of every valid configuration on MI355X.
   // Up to 16 tokens: 32-row tiles.  Where they fill at most one pass over
   // the CUs, one 8-wave workgroup per CU streams 16 KiB of weights per stage
   // (512-byte K slices, 3 stages ahead); with more rows, 2-wave workgroups
   // with 128-byte slices run six to a CU.  Below 16 rows per CU, 16-row tiles
   // split over 4 K groups.
-  // For 17-64 tokens a workgroup of 8 waves fills most of a CU's LDS, so one
-  // runs per CU: the tile height is the smallest of 32/64/96/128 rows whose
-  // grid fits in one pass over the CUs (taller tiles re-read the token tile
-  // less, shorter ones use more CUs); past 128 rows per CU, 64-row tiles keep
-  // the last pass's tail short.
+  // 17-64 tokens: the tile height and split from decode_plan.
   const int64_t cus = device_cus();
-  int per = 0;
-  const int sp = workspace ? decode_splits(M, N, K, cus, &per) : 1;
-  if (sp > 1) {
-    int32_t *part = static_cast<int32_t *>(workspace);
-    int32_t *part_rs = part + (int64_t)sp * M * N;
-    if (M <= 32)
-      return packed ? launch_decode_split<2, 8, 1, 1, 256, 3, true>(
-                          Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, sp, per, part, part_rs, st)
-                    : launch_decode_split<2, 8, 1, 1, 256, 3, false>(
-                          Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, sp, per, part, part_rs, st);
-    return packed ? launch_decode_split<4, 8, 1, 1, 256, 3, true>(
-                        Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, sp, per, part, part_rs, st)
-                  : launch_decode_split<4, 8, 1, 1, 256, 3, false>(
-                        Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, sp, per, part, part_rs, st);
-  }
   if (M <= 16) {
     if (N <= 16 * cus)
       return launch_decode<1, 1, 4, 1, 256, 4>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, packed, st);
@@ -500,21 +522,42 @@ hipError_t launch_qgemm_decode(const int8_t *Xq, const int8_t *Wq, const float *
       return launch_decode<1, 2, 4, 1, 512, 4>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, packed, st);
     return launch_decode<1, 2, 1, 1, 128, 4>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, packed, st);
   }
-  const int rows = N <= 32 * cus    ? 32
-                   : N <= 64 * cus  ? 64
-                   : N <= 96 * cus  ? 96
-                   : N <= 128 * cus ? 128
-                                    : 64;
-  if (M <= 32) {
-    if (rows == 32) return launch_decode<2, 2, 4, 1, 256, 4>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, packed, st);
-    if (rows == 64) return launch_decode<2, 4, 2, 1, 256, 3>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, packed, st);
-    if (rows == 96) return launch_decode<2, 2, 4, 3, 256, 3>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, packed, st);
-    return launch_decode<2, 8, 1, 1, 256, 3>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, packed, st);
+  // 17-64 tokens: one workgroup configuration per (token blocks, tile height),
+  // from a sweep of the valid configurations on MI355X
+  const DecodePlan p = decode_plan(M, N, K, cus, workspace != nullptr);
+  if (p.runs > 1) {
+    int32_t *part = static_cast<int32_t *>(workspace);
+    int32_t *part_rs = part + (int64_t)p.runs * M * N;
+#define OT_SPLIT(MB, NR, NK, RBW, BKD, S)                                                        \
+  return packed ? launch_decode_split<MB, NR, NK, RBW, BKD, S, true>(                              \
+                      Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, p.runs, p.per, part, part_rs, st) \
+                : launch_decode_split<MB, NR, NK, RBW, BKD, S, false>(                             \
+                      Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, p.runs, p.per, part, part_rs, st)
+    if (M <= 32) {
+      if (p.rows == 32) OT_SPLIT(2, 2, 4, 1, 256, 4);
+      if (p.rows == 64) OT_SPLIT(2, 4, 2, 1, 256, 4);
+      if (p.rows == 96) OT_SPLIT(2, 2, 4, 3, 256, 3);
+      OT_SPLIT(2, 4, 1, 2, 128, 4);
+    }
+    if (p.rows == 32) OT_SPLIT(4, 2, 4, 1, 256, 3);
+    if (p.rows == 64) OT_SPLIT(4, 4, 2, 1, 256, 3);
+    if (p.rows == 96) OT_SPLIT(4, 2, 4, 3, 256, 3);
+    OT_SPLIT(4, 8, 1, 1, 128, 4);
+#undef OT_SPLIT
   }
-  if (rows == 32) return launch_decode<4, 2, 4, 1, 256, 4>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, packed, st);
-  if (rows == 64) return launch_decode<4, 4, 2, 1, 256, 3>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, packed, st);
-  if (rows == 96) return launch_decode<4, 2, 4, 3, 256, 3>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, packed, st);
-  return launch_decode<4, 8, 1, 1, 256, 3>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, packed, st);
+#define OT_ONE(MB, NR, NK, RBW, BKD, S) \
+  return launch_decode<MB, NR, NK, RBW, BKD, S>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, packed, st)
+  if (M <= 32) {
+    if (p.rows == 32) OT_ONE(2, 2, 4, 1, 256, 4);
+    if (p.rows == 64) OT_ONE(2, 4, 2, 1, 256, 4);
+    if (p.rows == 96) OT_ONE(2, 2, 4, 3, 256, 3);
+    OT_ONE(2, 4, 1, 2, 128, 4);
+  }
+  if (p.rows == 32) OT_ONE(4, 2, 4, 1, 256, 3);
+  if (p.rows == 64) OT_ONE(4, 4, 2, 1, 256, 3);
+  if (p.rows == 96) OT_ONE(4, 2, 4, 3, 256, 3);
+  OT_ONE(4, 8, 1, 1, 128, 4);
+#undef OT_ONE
 }
 
 }  // namespace ot

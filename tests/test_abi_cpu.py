@@ -36,18 +36,24 @@ def test_strerror_and_version():
 
 
 def test_workspace_size_rule():
-    """Scratch only for the split-K decode path: 17..64 tokens and at most 32
-    output channels per compute unit (256 CUs without a GPU, as on MI355X);
-    runs x M x (N + 1) int32 for 2..8 runs of at least 4 K stages."""
+    """Scratch only where the decode launch plan splits K: 17..64 tokens,
+    runs x M x (N + 1) int32 for 2..8 runs (256 CUs without a GPU, as on
+    MI355X).  On the OPT-30B layers only fc2 splits."""
     ws = ot.ot_qlinear_workspace_size
-    for M, N, K in [(16, 7168, 7168), (65, 7168, 7168), (4096, 5120, 5120), (64, 21504, 7168),
-                    (64, 7168, 1024), (0, 7168, 7168), (64, 0, 7168), (64, 7168, 0)]:
+    for M, N, K in [(16, 7168, 28672), (65, 7168, 28672), (4096, 5120, 20480),
+                    (0, 7168, 7168), (64, 0, 7168), (64, 7168, 0),
+                    # OPT-30B qkv, out, fc1 at 32 and 64 tokens: one kernel
+                    (32, 21504, 7168), (64, 21504, 7168), (32, 7168, 7168), (64, 7168, 7168),
+                    (32, 28672, 7168), (64, 28672, 7168)]:
         assert ws(M, N, K) == 0, (M, N, K)
-    for M, N, K in [(17, 7168, 7168), (64, 7168, 28672), (33, 300, 4112), (64, 8192, 2048)]:
+    for M, N, K in [(17, 2048, 8192), (33, 300, 4112), (40, 2048, 9216), (63, 8192, 9216),
+                    (17, 9216, 16384)]:
         n = ws(M, N, K)
         unit = M * (N + 1) * 4
         assert n % unit == 0 and 2 <= n // unit <= 8, (M, N, K, n)
-    assert ws(64, 7168, 7168) == 4 * 64 * 7169 * 4  # 56 row tiles of 128 x 4 runs of 7 stages
+    # OPT-30B fc2: 64-row tiles x 2 runs at 32 tokens, 96-row x 3 at 64
+    assert ws(32, 7168, 28672) == 2 * 32 * 7169 * 4
+    assert ws(64, 7168, 28672) == 3 * 64 * 7169 * 4
 
 
 NULL = None

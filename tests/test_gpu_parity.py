@@ -160,10 +160,10 @@ QL_SHAPES = [
     (32, 513, 128), (33, 64, 48), (64, 1000, 2064),
     # decode kernel, every tile for up to 16 tokens (16-row tiles up to
     # N = 4096, 32-row tiles with 512-byte K slices up to 8192, 32-row tiles
-    # with 128-byte slices beyond) and every tile height for 17-64 tokens (32
-    # rows up to N = 8192, 64 rows up to 16384, 96 rows up to 24576, 128 rows
-    # up to 32768, 64 rows beyond), on both sides of each boundary, with
-    # ragged N and K tails
+    # with 128-byte slices beyond) and, for 17-32 and 33-64 tokens, every
+    # tile height the unsplit launch plan picks (32, 64, 96 and 128 rows
+    # while a grid fits one pass over 256 CUs, 64 rows beyond), on both sides
+    # of the one-pass boundaries, with ragged N and K tails
     (1, 4096, 528), (2, 4097, 1040), (3, 7168, 1040), (16, 5000, 2064), (8, 8192, 48),
     (1, 16400, 272), (9, 16384, 2064), (20, 16448, 528), (64, 16392, 784),
     (32, 8192, 512), (48, 8193, 96), (17, 8195, 2000), (33, 12000, 1040),
@@ -292,8 +292,11 @@ def test_prefill_tiles_staged_epilogue(M, N, K, flavour):
 # need no initialization); outputs must match the oracle and, bit for bit,
 # the call without a workspace.
 # --------------------------------------------------------------------------
-SPLIT_SHAPES = [(17, 7168, 7168), (32, 5000, 4112), (33, 300, 4112), (48, 8192, 2064),
-                (64, 7168, 28672)]
+# Split-K plans on 256 CUs (tile height x K runs): 17-32 tokens 32 x 3,
+# 64 x 2 (OPT-30B fc2), 96 x 2; 33-64 tokens 32 x 4, 64 x 6, 96 x 3 (OPT-30B
+# fc2), 128 x 3 (128-byte K stages)
+SPLIT_SHAPES = [(17, 2048, 8192), (32, 7168, 28672), (17, 9216, 16384), (33, 300, 4112),
+                (40, 2048, 9216), (64, 7168, 28672), (63, 8192, 9216)]
 
 
 @pytest.mark.parametrize("M,N,K", SPLIT_SHAPES)
@@ -332,7 +335,7 @@ def test_decode_split_k(M, N, K, flavour):
 
 
 def test_workspace_too_small_is_rejected_by_the_binding():
-    M, N, K = 32, 7168, 7168
+    M, N, K = 32, 7168, 28672
     Xq, Wq, sW, bp = (dev(a) for a in _random_qlinear_inputs(M, N, K, 8, 8, 5))
     small = torch.empty(ot.ot_qlinear_workspace_size(M, N, K) - 16, dtype=torch.uint8,
                         device="cuda")
@@ -349,7 +352,7 @@ def test_workspace_too_small_is_rejected_by_the_binding():
 # no state between calls).
 # --------------------------------------------------------------------------
 def test_graph_replay_matches_eager():
-    shapes = [(300, 772, 1040), (8, 7168, 2064), (48, 7168, 2064)]
+    shapes = [(300, 772, 1040), (8, 7168, 2064), (40, 2048, 4112)]
     calls = []
     for i, (M, N, K) in enumerate(shapes):
         Xq, Wq, sW, bp = (dev(a) for a in _random_qlinear_inputs(M, N, K, 8, 8, 100 + i))
