@@ -478,20 +478,29 @@ def traffic_record(d, workload):
 
 def decode_probe(torch, ot, synth, wl, pool):
     """Each decode-regime linear once per token count, in a fixed order
-    (M ascending, then qkv, out, fc1, fc2), as the bench runs it (workspace
-    where the library uses one); for counter runs."""
+    (row-major weights, then packed; M ascending; qkv, out, fc1, fc2), as
+    the bench runs it (workspace where the library uses one); for counter
+    runs."""
     layers = prepare(wl, max(wl.decode_M), torch, ot, synth, pool)
+    for L in layers:
+        L["Wp"] = ot.pack_weights(L["Wq"])
     plan = []
-    for M in wl.decode_M:
-        for L in layers:
-            xq = ot.quantize_act(L["X"][:M].contiguous(), wl.a_bits, L["z"], L["inv_s"])
-            y = torch.empty((M, L["N"]), dtype=torch.float16, device="cuda")
-            plan.append((M, L, xq, y, ot.workspace_for(M, L["N"], L["K"])))
+    for packed in (False, True):
+        for M in wl.decode_M:
+            for L in layers:
+                xq = ot.quantize_act(L["X"][:M].contiguous(), wl.a_bits, L["z"], L["inv_s"])
+                y = torch.empty((M, L["N"]), dtype=torch.float16, device="cuda")
+                plan.append((packed, M, L, xq, y, ot.workspace_for(M, L["N"], L["K"])))
     torch.cuda.synchronize()
-    for M, L, xq, y, ws in plan:
-        ot.ot_qlinear(xq, L["Wq"], L["sW"], L["bp"], wl.a_bits, wl.w_bits, y, workspace=ws)
+    for packed, M, L, xq, y, ws in plan:
+        if packed:
+            ot.ot_qlinear_packed(xq, L["Wp"], L["N"], L["sW"], L["bp"], wl.a_bits, wl.w_bits, y,
+                                 workspace=ws)
+        else:
+            ot.ot_qlinear(xq, L["Wq"], L["sW"], L["bp"], wl.a_bits, wl.w_bits, y, workspace=ws)
     torch.cuda.synchronize()
-    print(json.dumps({"decode_probe": [[M, L["name"], ws is not None] for M, L, _, _, ws in plan]}))
+    print(json.dumps({"decode_probe": [[p, M, L["name"], ws is not None]
+                                       for p, M, L, _, _, ws in plan]}))
 
 
 def counter_summary(d, workload, decode_workload):
@@ -544,11 +553,12 @@ def counter_summary(d, workload, decode_workload):
     wr_f = n_copy / float(np.median([e["TCC_EA0_WRREQ_WRITE_DRAM_32B"] * 32 for e in big]))
     dwl = synth.WORKLOADS[decode_workload]
     dec = [e for e in dispatches("dram") if "qgemm_decode" in e["name"] or "decode_reduce" in e["name"]]
-    order = [(M, L) for M in dwl.decode_M for L in dwl.layers]
-    out2 = ["| M | Layer | kernels | DRAM read bytes | DRAM write bytes | algorithmic bytes | read / algorithmic |",
-            "|---|---|---|---|---|---|---|"]
+    order = [(p, M, L) for p in ("row-major", "packed") for M in dwl.decode_M
+             for L in dwl.layers]
+    out2 = ["| Weights | M | Layer | kernels | DRAM read bytes | DRAM write bytes | algorithmic bytes | read / algorithmic |",
+            "|---|---|---|---|---|---|---|---|"]
     i = 0
-    for M, L in order:
+    for p, M, L in order:
         ks = [dec[i]]
         i += 1
         if "split" in ks[0]["name"]:
@@ -557,7 +567,7 @@ def counter_summary(d, workload, decode_workload):
         rd = sum(e["TCC_EA0_RDREQ_DRAM_32B"] for e in ks) * 32 * rd_f
         wr = sum(e["TCC_EA0_WRREQ_WRITE_DRAM_32B"] for e in ks) * 32 * wr_f
         alg = L.K * L.N + M * L.K + 2 * M * L.N + 8 * L.N
-        out2.append(f"| {M} | {L.name} | {len(ks)} | {rd / 1e6:.1f} MB | {wr / 1e6:.2f} MB | "
+        out2.append(f"| {p} | {M} | {L.name} | {len(ks)} | {rd / 1e6:.1f} MB | {wr / 1e6:.2f} MB | "
                     f"{alg / 1e6:.1f} MB | {rd / alg:.3f} |")
     if i != len(dec):
         raise SystemExit(f"{len(dec)} decode dispatches, {i} accounted for")
