@@ -8,12 +8,12 @@ namespace ot {
 namespace detail {
 
 // ---------------------------------------------------------------------------
-// Shared-token ring: one LDS ring for tokens and weights
+// Shared-token ring: one LDS ring for tokens and (row-major) weights
 // ---------------------------------------------------------------------------
 // Loading the token fragments into every wave's registers would limit how
 // far ahead a wave can fetch (and repeat the token loads per wave).  The
 // NW = NR x NK waves of a workgroup step through K together over one ring of
-// S stages.  A stage
+// S stages (packed weights bypass it: decode_body_packed).  A stage
 // holds the token tile [16*MB rows][BKD] and the workgroup's weight tile
 // [16*RBW*NR rows][BKD], both filled by buffer load-to-LDS S-1 stages ahead
 // with the loads spread evenly over all waves; one barrier per stage.  Wave
@@ -721,6 +721,16 @@ hipError_t launch_qgemm_decode(const int8_t *Xq, const int8_t *Wq, const float *
   // 17-64 tokens: the tile height and split from decode_plan, the tile
   // configuration from decode_tiles.
   const int64_t cus = device_cus();
+  if (M <= 16 && packed) {
+    // packed weights stream into registers and the LDS ring holds only the
+    // token rows, so deeper rings win: from a sweep of 23 configurations on
+    // 14 layer shapes (N = 4096 .. 36864) at 1, 8 and 16 tokens
+    if (N <= 16 * cus)
+      return launch_decode_t<1, 1, 4, 1, 256, 8, true>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, st);
+    if (N <= 32 * cus || N > 64 * cus)
+      return launch_decode_t<1, 2, 1, 1, 128, 8, true>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, st);
+    return launch_decode_t<1, 2, 1, 2, 128, 6, true>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, st);
+  }
   if (M <= 16) {
     if (N <= 16 * cus)
       return launch_decode<1, 1, 4, 1, 256, 4>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y, acc_out, packed, st);
