@@ -683,12 +683,14 @@ static hipError_t decode_tiles(const DecodePlan &p, const int8_t *Xq, const int8
   return decode_tile<MB, NR, NK, RBW, BKD, S, PACKED>(p.runs, Xq, Wq, sX, zW, sW, bp, M, N, K, \
                                                       Y, acc_out, part, part_rs, st)
   if (M <= 32) {
-    if (p.rows == 32) OT_TILE(2, 2, 4, 1, 256, 4);
-    if (p.rows == 64) OT_TILE(2, 4, 2, 1, 256, 4);
     if constexpr (PACKED) {
+      if (p.rows == 32) OT_TILE(2, 2, 1, 1, 128, 8);
+      if (p.rows == 64) OT_TILE(2, 4, 1, 1, 128, 8);
       if (p.rows == 96) OT_TILE(2, 2, 4, 3, 256, 4);
       OT_TILE(2, 8, 1, 1, 256, 3);
     } else {
+      if (p.rows == 32) OT_TILE(2, 2, 4, 1, 256, 4);
+      if (p.rows == 64) OT_TILE(2, 4, 2, 1, 256, 4);
       if (p.rows == 96) OT_TILE(2, 2, 4, 3, 256, 3);
       OT_TILE(2, 4, 1, 2, 128, 4);
     }
