@@ -122,12 +122,22 @@ def test_decode_layer_full(name, li):
     assert np.array_equal(g["Xq_dev"].cpu().numpy(), rXq)
     racc = O.int_gemm(rXq, rWq)  # all 64 tokens x all channels
     rY = O.epilogue(racc, rsW, rbp)
+    Wp = ot.pack_weights(g["Wq_dev"])
     for M in wl.decode_M:
-        Y = ot.qlinear(g["Xq_dev"][:M].contiguous(), g["Wq_dev"], g["sW_dev"], g["bp_dev"],
-                       wl.a_bits, wl.w_bits)
-        Y2, acc = ot.qlinear(g["Xq_dev"][:M].contiguous(), g["Wq_dev"], g["sW_dev"],
-                             g["bp_dev"], wl.a_bits, wl.w_bits, want_acc=True)
+        Xm = g["Xq_dev"][:M].contiguous()
+        Y = ot.qlinear(Xm, g["Wq_dev"], g["sW_dev"], g["bp_dev"], wl.a_bits, wl.w_bits)
+        Y2, acc = ot.qlinear(Xm, g["Wq_dev"], g["sW_dev"], g["bp_dev"], wl.a_bits, wl.w_bits,
+                             want_acc=True)
+        # the benchmark's launches: a workspace (split K where the plan takes
+        # it), on row-major and on packed weights
+        Y3, acc3 = ot.qlinear(Xm, g["Wq_dev"], g["sW_dev"], g["bp_dev"], wl.a_bits, wl.w_bits,
+                              want_acc=True, workspace=True)
+        Y4, acc4 = ot.qlinear_packed(Xm, Wp, lay.N, g["sW_dev"], g["bp_dev"], wl.a_bits,
+                                     wl.w_bits, want_acc=True, workspace=True)
         torch.cuda.synchronize()
         assert np.array_equal(acc.cpu().numpy(), racc[:M]), f"acc M={M}"
+        assert np.array_equal(acc3.cpu().numpy(), racc[:M]), f"acc (workspace) M={M}"
+        assert np.array_equal(acc4.cpu().numpy(), racc[:M]), f"acc (packed) M={M}"
         assert_fp16_close(Y.cpu().numpy(), rY[:M], f"Y M={M}")
         assert_fp16_close(Y2.cpu().numpy(), rY[:M], f"Y(acc path) M={M}")
+        assert torch.equal(Y3, Y) and torch.equal(Y4, Y), f"Y (workspace, packed) M={M}"
