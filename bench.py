@@ -412,6 +412,33 @@ def _per_dispatch(rows, name_part):
     return [(grid[d], acc[d]) for d in sorted(acc)]
 
 
+def prefill_fetch_floor(M, N, K, bn, bm, group_m=8, xcds=8, per_xcd=32):
+    """Least HBM-side operand fetch (bytes) of one prefill launch under the
+    kernel's tile schedule: the workgroups are dealt to the XCDs in
+    contiguous ranges and walked in groups of group_m token tiles, and each
+    XCD runs per_xcd of them at a time (one per CU); its L2 can share the
+    operand panels only among those, so per XCD and pass every distinct
+    token panel (bm rows) and channel panel (bn rows) is fetched over all of
+    K once."""
+    tiles_m, tiles_n = -(-M // bm), -(-N // bn)
+    nwg = tiles_m * tiles_n
+    per, rem = nwg // xcds, nwg % xcds
+    total = 0
+    for x in range(xcds):
+        n_x = per + (1 if x < rem else 0)
+        start = x * (per + 1) if x < rem else rem * (per + 1) + (x - rem) * per
+        for p0 in range(start, start + n_x, per_xcd):
+            tms, tns = set(), set()
+            for lid in range(p0, min(p0 + per_xcd, start + n_x)):
+                gs = group_m * tiles_n
+                first_m = (lid // gs) * group_m
+                gm = min(tiles_m - first_m, group_m)
+                tms.add(first_m + (lid % gs) % gm)
+                tns.add((lid % gs) // gm)
+            total += (len(tms) * bm + len(tns) * bn) * K
+    return total
+
+
 def traffic_record(d, workload):
     """Writes the prefill GEMM's HBM traffic record from four rocprofv3 --pmc
     runs under d: fetch/ and write/ (FETCH_SIZE, WRITE_SIZE of `bench.py
@@ -447,8 +474,10 @@ def traffic_record(d, workload):
     for L in wl.layers:
         f = float(np.mean(per[L.name]["fetch_kib"]))
         w = float(np.mean(per[L.name]["write_kib"]))
+        bn, bm = (int(v) for v in tile_of[L.name].split("x"))
         rec_layers[L.name] = {"fetch_kib": f, "write_kib": w, "tile": tile_of[L.name],
-                              "bytes": (f * factors["FETCH_SIZE"] + w * factors["WRITE_SIZE"]) * 1024}
+                              "bytes": (f * factors["FETCH_SIZE"] + w * factors["WRITE_SIZE"]) * 1024,
+                              "fetch_floor_bytes": prefill_fetch_floor(wl.M, L.N, L.K, bn, bm)}
         alg[L.name] = wl.M * L.K + L.N * L.K + 2 * wl.M * L.N + 8 * L.N
     cmd = "cd /tmp && timeout -s KILL 120 rocprofv3 --pmc {c} --output-format csv -d <out>/{sub} -o p -- python -u <repo>/bench.py {args}"
     bench_args = ("--steps 2 --warmup 1 --no-cpu --no-fp16 --no-decode --no-ln --no-mixed "
