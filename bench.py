@@ -537,8 +537,9 @@ def counter_summary(d, workload, decode_workload):
     mfma/ (SQ_INSTS_VALU_MFMA_MOPS_I8, SQ_VALU_MFMA_BUSY_CYCLES,
     SQ_BUSY_CU_CYCLES, GRBM_GUI_ACTIVE, SQ_LDS_BANK_CONFLICT, SQ_INSTS_LDS
     over the prefill step), dram/ (TCC_EA0_RDREQ_DRAM_32B,
-    TCC_EA0_WRREQ_WRITE_DRAM_32B over --decode-probe) and dram_copy/ (the
-    same over --copy-probe).  rocprofv3 sums each counter over its hardware
+    TCC_EA0_WRREQ_WRITE_DRAM_32B over --decode-probe), dram_copy/ (the
+    same over --copy-probe) and, if present, dram_prefill/ (the same over
+    the prefill step).  rocprofv3 sums each counter over its hardware
     instances; GRBM_GUI_ACTIVE is counted once per XCD, so it is divided by
     the 8 XCDs."""
     import csv
@@ -600,11 +601,28 @@ def counter_summary(d, workload, decode_workload):
                     f"{alg / 1e6:.1f} MB | {rd / alg:.3f} |")
     if i != len(dec):
         raise SystemExit(f"{len(dec)} decode dispatches, {i} accounted for")
+    out3 = []
+    if os.path.isdir(os.path.join(d, "dram_prefill")):
+        pre_d = [e for e in dispatches("dram_prefill") if "qgemm_prefill_kernel" in e["name"]]
+        out3 = ["| Layer | DRAM read bytes | DRAM write bytes | algorithmic reads (Xq + Wq + sW + b') | reads / algorithmic |",
+                "|---|---|---|---|---|"]
+        for li, L in enumerate(wl.layers):
+            es = pre_d[li::len(wl.layers)]
+            rd = np.mean([e["TCC_EA0_RDREQ_DRAM_32B"] for e in es]) * 32 * rd_f
+            wr = np.mean([e["TCC_EA0_WRREQ_WRITE_DRAM_32B"] for e in es]) * 32 * wr_f
+            alg = wl.M * L.K + L.N * L.K + 8 * L.N
+            out3.append(f"| {L.name} | {rd / 1e6:.1f} MB | {wr / 1e6:.1f} MB | {alg / 1e6:.1f} MB | "
+                        f"{rd / alg:.3f} |")
     print("\n".join(out))
     print()
     print(f"DRAM counter calibration on a 1 GiB copy: read factor {rd_f:.3f}, write factor {wr_f:.3f}")
     print()
     print("\n".join(out2))
+    if out3:
+        print()
+        print("Prefill step (OPT-13B W6A6), DRAM bytes per launch:")
+        print()
+        print("\n".join(out3))
 
 
 def copy_probe(torch):
