@@ -293,9 +293,10 @@ __device__ __forceinline__ void decode_body(
 // of the run every load is out of range and returns zeros, so the loop runs
 // whole groups of S stages and the extra ones add nothing.  The vmcnt waits
 // are counted by hand over the program order of the loads, so the weight
-// pointer carries no __restrict__: the compiler then keeps the register
-// loads in place around the barriers (which clobber memory) instead of
-// sinking them past a wait.
+// pointer carries no __restrict__ and a compiler fence closes each stage's
+// group of loads: a register load from memory the compiler may not assume
+// unchanged then stays between the fences and barriers (which clobber
+// memory) around it, instead of moving past a wait.
 template <int MB, int NR, int NK, int RBW, int BKD, int S, int EPI, bool SPLIT>
 __device__ __forceinline__ void decode_body_packed(
     int8_t *smem, const int8_t *__restrict__ Xq, const int8_t *Wp,
