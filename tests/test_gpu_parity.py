@@ -359,14 +359,25 @@ def test_graph_replay_matches_eager():
         Y = torch.empty((M, N), dtype=torch.float16, device="cuda")
         calls.append((Xq, Wq, sW, bp, Y, ot.workspace_for(M, N, K)))
     assert calls[2][5] is not None, "the last shape takes the split-K path"
-    case("graph replay of prefill, decode and split-K decode")
+    # the split-K decode once more on packed weights (registers streamed
+    # from the packed layout), into its own output and workspace
+    Xq, Wq, sW, bp = calls[2][:4]
+    Wp = ot.pack_weights(Wq)
+    M, N, K = Xq.shape[0], Wq.shape[0], Wq.shape[1]
+    packed = (Xq, Wp, N, sW, bp, torch.empty((M, N), dtype=torch.float16, device="cuda"),
+              ot.workspace_for(M, N, K))
+    case("graph replay of prefill, decode, split-K decode and packed split-K decode")
 
     def run():
         for Xq, Wq, sW, bp, Y, ws in calls:
             ot.ot_qlinear(Xq, Wq, sW, bp, 8, 8, Y, workspace=ws)
+        Xq, Wp, N, sW, bp, Y, ws = packed
+        ot.ot_qlinear_packed(Xq, Wp, N, sW, bp, 8, 8, Y, workspace=ws)
     run()
     torch.cuda.synchronize()
-    ref = [c[4].clone() for c in calls]
+    assert torch.equal(packed[5], calls[2][4])
+    outs = [c[4] for c in calls] + [packed[5]]
+    ref = [y.clone() for y in outs]
     g = torch.cuda.CUDAGraph()
     s = torch.cuda.Stream()
     s.wait_stream(torch.cuda.current_stream())
@@ -376,14 +387,14 @@ def test_graph_replay_matches_eager():
     torch.cuda.current_stream().wait_stream(s)
     other = torch.randn(1 << 20, device="cuda")
     for rep in range(4):
-        for c in calls:
-            c[4].zero_()
+        for y in outs:
+            y.zero_()
         other.mul_(1.0001)  # eager work between replays
         torch.cuda.synchronize()
         g.replay()
         torch.cuda.synchronize()
-        for c, r in zip(calls, ref):
-            assert torch.equal(c[4], r), f"replay {rep} differs from the eager outputs"
+        for y, r in zip(outs, ref):
+            assert torch.equal(y, r), f"replay {rep} differs from the eager outputs"
 
 
 # --------------------------------------------------------------------------
