@@ -296,9 +296,10 @@ size_t ot_qlinear_workspace_size(int64_t M, int64_t N, int64_t K);
 
 /*
  * Packed weights for decode.  The folded codes (Eq. (f) right-hand side,
- * fixed offline like the fold itself, Sec. 3.2) re-laid so that the
- * weight-streaming kernel reads them as contiguous runs: 1 KiB micro-tiles
- * of 16 output channels by 64 input channels,
+ * fixed offline like the fold itself, Sec. 3.2) re-laid so that each 1 KiB
+ * is one matrix-instruction operand of a wave, which the weight-streaming
+ * kernel loads straight into registers: micro-tiles of 16 output channels
+ * by 64 input channels,
  *   Wp[g][s][l][b] = Wq[16 g + (l mod 16)][64 s + 16 (l / 16) + b]
  * for g < ceil(N/16), s < ceil(K/64), lane l < 64, byte b < 16, and 0 where
  * the row is >= N or the column >= K (the lane order of the A operand of
