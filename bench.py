@@ -51,6 +51,8 @@ def parse():
     p.add_argument("--no-decode", action="store_true", help="skip the decode-regime report")
     p.add_argument("--no-fp16", action="store_true", help="skip the fp16 torch baseline")
     p.add_argument("--no-cpu", action="store_true", help="skip the CPU-oracle baseline")
+    p.add_argument("--no-sclk", action="store_true",
+                   help="skip the shader-clock window (about 1 s of untimed prefill steps)")
     p.add_argument("--no-ln", action="store_true", help="skip the fused LayerNorm report")
     p.add_argument("--no-asym", action="store_true",
                    help="skip the asymmetric-weight step report")
@@ -481,7 +483,7 @@ def traffic_record(d, workload):
         alg[L.name] = wl.M * L.K + L.N * L.K + 2 * wl.M * L.N + 8 * L.N
     cmd = "cd /tmp && timeout -s KILL 120 rocprofv3 --pmc {c} --output-format csv -d <out>/{sub} -o p -- python -u <repo>/bench.py {args}"
     bench_args = ("--steps 2 --warmup 1 --no-cpu --no-fp16 --no-decode --no-ln --no-mixed "
-                  "--no-asym")
+                  "--no-asym --no-sclk")
     rec = {
         "kernel": "qgemm_prefill_kernel (256x256, 320x256 or 256x128 tiles, BK 128, 2 stages)",
         "workload": f"{wl.name} ({wl.M} tokens; " + ", ".join(L.name for L in wl.layers) + ")",
@@ -681,6 +683,58 @@ def cpu_baseline(ot_oracle, layers, M, budget_s=10.0):
 
 
 # ---------------------------------------------------------------------------
+def shader_clock_window(torch, step, seconds=1.0):
+    """The shader clock while the prefill step runs back to back for about
+    `seconds` (outside the timed region): the per-XCD current gfx clocks of
+    the SMU's metrics table, read in-process through the amdsmi library
+    every 5 ms by a thread (no subprocess), idle readings (< 500 MHz)
+    dropped.  Returns an "error" entry instead where the library is
+    missing or refuses."""
+    import threading
+    try:
+        import amdsmi
+        amdsmi.amdsmi_init(amdsmi.AmdSmiInitFlags.INIT_AMD_GPUS)
+    except Exception as e:  # no SMI library or no access: report, do not fail
+        return {"error": f"amdsmi unavailable: {e}"}
+    try:
+        h = amdsmi.amdsmi_get_processor_handles()[0]
+        samples, stop = [], threading.Event()
+
+        def sample():
+            while not stop.is_set():
+                clks = amdsmi.amdsmi_get_gpu_metrics_info(h).get("current_gfxclks")
+                if isinstance(clks, list):
+                    samples.append([c for c in clks if isinstance(c, int) and c >= 500])
+                stop.wait(0.005)
+
+        th = threading.Thread(target=sample, daemon=True)
+        th.start()
+        t0, runs = time.perf_counter(), 0
+        while time.perf_counter() - t0 < seconds:
+            for _ in range(10):
+                step()
+            torch.cuda.synchronize()
+            runs += 10
+        stop.set()
+        th.join()
+        flat = [c for row in samples for c in row]
+        if not flat:
+            return {"error": "no clock readings above idle"}
+        per_xcd = [float(np.median([row[i] for row in samples if len(row) > i]))
+                   for i in range(max(len(r) for r in samples))]
+        return {"median_MHz": float(np.median(flat)), "p10_MHz": float(np.percentile(flat, 10)),
+                "p90_MHz": float(np.percentile(flat, 90)), "per_xcd_median_MHz": per_xcd,
+                "readings": len(samples), "steps": runs,
+                "source": "amdsmi gpu metrics current_gfxclks, every 5 ms over back-to-back steps"}
+    except Exception as e:
+        return {"error": f"amdsmi read failed: {e}"}
+    finally:
+        try:
+            amdsmi.amdsmi_shut_down()
+        except Exception:
+            pass
+
+
 def main():
     args = parse()
     if args.traffic_record:
@@ -783,6 +837,19 @@ def main():
         "quantize_act_ms_per_step": round(ms_step - gemm_ms, 4),
         "tokens_per_s": round(M / (ms_step * 1e-3), 1),
     }
+    if not args.no_sclk:
+        clk = shader_clock_window(torch, step)
+        if "median_MHz" in clk:
+            # the matrix cores' peak scales with the clock (5.0 POP/s at 2400 MHz)
+            peak_at_clk = PEAK_INT8_TOPS * clk["median_MHz"] / 2400.0
+            clk["frac_of_2400_MHz"] = round(clk["median_MHz"] / 2400.0, 4)
+            clk["qlinear_frac_of_mfma_peak_at_this_clock"] = round(gemm_tops / peak_at_clk, 4)
+            log(f"shader clock over {clk['steps']} steps: median {clk['median_MHz']:.0f} MHz; "
+                f"qlinear at {100 * clk['qlinear_frac_of_mfma_peak_at_this_clock']:.0f} % of the "
+                f"MFMA peak at that clock")
+        else:
+            log(f"shader clock: {clk['error']}")
+        result["prefill_shader_clock"] = clk
     if not args.no_fp16:
         fb = fp16_baseline(torch, layers, M, args.iters)
         fb["speedup_of_step"] = fb["ms_per_stack"] / ms_step
