@@ -56,6 +56,32 @@ def test_workspace_size_rule():
     assert ws(64, 7168, 28672) == 3 * 64 * 7169 * 4
 
 
+def test_workspace_size_properties_over_random_shapes():
+    """Every split the launch plan picks (17..64 tokens, 256 CUs without a
+    GPU): 2..8 runs of at least 1 KiB of K each, on a grid that fits one
+    pass over the CUs for some tile height (32..128 rows); never a split
+    outside 17..64 tokens."""
+    import numpy as np
+    r = np.random.default_rng(7)
+    ws = ot.ot_qlinear_workspace_size
+    for _ in range(400):
+        M = int(r.integers(1, 129))
+        N = int(r.integers(1, 40000))
+        K = int(r.integers(1, 3000)) * 16
+        n = ws(M, N, K)
+        if not 17 <= M <= 64:
+            assert n == 0, (M, N, K)
+            continue
+        if n == 0:
+            continue
+        unit = M * (N + 1) * 4
+        assert n % unit == 0, (M, N, K, n)
+        runs = n // unit
+        assert 2 <= runs <= 8, (M, N, K, runs)
+        assert (K + 255) // 256 >= 4 * runs, (M, N, K, runs)
+        assert any(-(-N // rows) * runs <= 256 for rows in (32, 64, 96, 128)), (M, N, K, runs)
+
+
 NULL = None
 
 
