@@ -44,8 +44,8 @@ PEAK_HBM_GBS = 8000.0      # MI355X HBM3E, 8 TB/s
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=20)
-    p.add_argument("--warmup", type=int, default=5)
+    p.add_argument("--steps", type=int, default=50)
+    p.add_argument("--warmup", type=int, default=10)
     p.add_argument("--workload", default="opt13b_w6a6")
     p.add_argument("--decode-workload", default="opt30b_decode_w8a8")
     p.add_argument("--no-decode", action="store_true", help="skip the decode-regime report")
