@@ -180,10 +180,12 @@ hipError_t launch_ln_quantize_act(const uint16_t *h, int64_t M, int64_t K, const
                                   const uint16_t *beta, float eps, int qa, const float *z,
                                   const float *inv_s, int8_t *Xq, hipStream_t st) {
   // one row per workgroup, 4 chunks of 8 channels per thread up to
-  // K = 4096 and 8 beyond (a workgroup of at most 1024 threads covers
-  // K = 65536); measured on K = 768 ... 32768 against 2, 16 and 32 chunks
-  // per thread and 2 rows per workgroup
-  if (K <= 4096) return launch_lnq<4, 1>(h, M, K, gamma, beta, eps, qa, z, inv_s, Xq, st);
+  // K = 2048 and 8 beyond (a workgroup of at most 1024 threads covers
+  // K = 65536); measured on K = 768 ... 32768 against 2 to 32 chunks per
+  // thread, 1 or 2 rows per workgroup and two launch bounds (8 chunks is
+  // 10 % faster than 4 at K = 4096 and within 2 % of the best from 3072 to
+  // 9216)
+  if (K <= 2048) return launch_lnq<4, 1>(h, M, K, gamma, beta, eps, qa, z, inv_s, Xq, st);
   return launch_lnq<8, 1>(h, M, K, gamma, beta, eps, qa, z, inv_s, Xq, st);
 }
 

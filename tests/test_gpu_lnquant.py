@@ -79,7 +79,8 @@ def _run(H, gamma, beta, eps, a_bits, z, inv_s):
 
 # widths on both sides of the 16384 / 32768 kernel-configuration boundaries,
 # ragged against the 8-channel chunks and the 64-thread waves
-SHAPES = [(1, 16), (3, 768), (17, 1040), (130, 512), (64, 4096), (9, 5120), (5, 16384),
+SHAPES = [(1, 16), (3, 768), (17, 1040), (130, 512), (4, 2048), (7, 2064), (64, 4096),
+          (9, 5120), (5, 16384),
           (2, 16400), (3, 32768), (2, 32784), (1, 65536)]
 
 
