@@ -891,6 +891,16 @@ def main():
         result["decode"] = {"workload": dwl.name, "bound": "hbm", "peak_GBps": PEAK_HBM_GBS,
                             "by_M": decode_report(torch, ot, synth, dwl, pool, args.iters,
                                                   not args.no_fp16)}
+        # per token count, the faster of the two weight layouts (eager launches)
+        summ = {}
+        for m, r in result["decode"]["by_M"].items():
+            packed = r.get("packed_us_per_stack")
+            best = "packed" if packed is not None and packed < r["us_per_stack"] else "row-major"
+            us = packed if best == "packed" else r["us_per_stack"]
+            gbs = r["bytes_per_stack"] / (us * 1e-6) / 1e9
+            summ[m] = {"weights": best, "us_per_stack": round(us, 2), "GBps": round(gbs, 1),
+                       "frac_of_hbm_peak": round(gbs / PEAK_HBM_GBS, 4)}
+        result["decode"]["best_layout_by_M"] = summ
         torch.cuda.empty_cache()
         result["decode"]["hbm_copy_context"] = hbm_copy_context(torch)
         log(f"plain 1 GiB device copy: {result['decode']['hbm_copy_context']['GBps']:.0f} GB/s "
