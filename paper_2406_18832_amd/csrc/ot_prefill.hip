@@ -131,9 +131,20 @@ __device__ __forceinline__ void prefill_body(
     off_b[j] = (uint32_t)(row * K + ck_b[j] * 16);
   }
   const int KT = (K + BK - 1) / BK;
+  // Neighbouring tiles (a checkerboard over token x channel tiles) walk K
+  // one tile apart, the odd ones starting at K tile 1 and wrapping round to
+  // 0, so that the tiles sharing operand panels in an XCD's L2 do not all
+  // ask for the same lines at once.  The accumulators are exact integer
+  // sums, which do not depend on the order.
+  const int phi = (tm + tn) & 1;
 
   auto issue_tile = [&](int kt) {
-    const int k0 = kt * BK;  // every chunk of a tile kt >= KT is out of range
+    int kr = kt;  // the K tile that iteration kt loads
+    if (kt < KT) {
+      kr = kt + phi;
+      if (kr >= KT) kr -= KT;
+    }
+    const int k0 = kr * BK;  // iterations kt >= KT load only out-of-range chunks
     int8_t *sa = smem + (kt % S) * C::kStage;
     int8_t *sb = sa + C::kABytes;
 #pragma unroll
