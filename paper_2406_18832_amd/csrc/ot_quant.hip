@@ -4,9 +4,10 @@
 //   Xq[m, k] = clip(rne(fp32(fp32(x[m, k]) - z_k) * inv_s_k), -qa, qa)
 //
 // HBM-bound streaming kernel: 2 bytes in, 1 byte out per element.  A wave
-// covers 64 x 16 = 1024 consecutive channels of one row (32-byte loads and
-// 16-byte stores per lane, fully coalesced) and keeps those channels' z and
-// inv_s in registers while it walks down kRowsPerWave rows.
+// covers 64 x 8 = 512 consecutive channels (16-byte loads and 8-byte stores
+// per lane, fully coalesced), keeps those channels' z and inv_s in registers
+// and takes kRowsPerWave consecutive rows at a time, all of their loads
+// issued before any arithmetic.
 //
 // Also here: the dynamic per-token quantizer of Eq. (c) for the linears that
 // the paper leaves per-token (out, fc2).
@@ -16,7 +17,10 @@ namespace ot {
 namespace detail {
 
 constexpr int kWavesPerBlock = 4;
-constexpr int kRowsPerWave = 4;  // measured best of 1..16 on 4096 x 5120, 4096 x 20480, 8192 x 9216
+constexpr int kChannelsPerLane = 8;
+// From a sweep on MI355X of 8 or 16 channels per lane, 4-64 rows per wave and
+// 1-16 rows' loads in flight, over 2048-8192 rows by 4096-36864 channels
+constexpr int kRowsPerWave = 4;
 
 __device__ inline uint32_t pack4(int a, int b, int c, int d) {
   return (uint32_t)(a & 0xff) | ((uint32_t)(b & 0xff) << 8) | ((uint32_t)(c & 0xff) << 16) |
@@ -26,37 +30,41 @@ __device__ inline uint32_t pack4(int a, int b, int c, int d) {
 __global__ __launch_bounds__(64 * kWavesPerBlock) void quantize_act_kernel(
     const uint16_t *__restrict__ x, int64_t M, int64_t K, float qa, const float *__restrict__ z,
     const float *__restrict__ inv_s, int8_t *__restrict__ Xq) {
-  const int64_t chunk = (int64_t)blockIdx.x * 64 + threadIdx.x;  // 16-channel chunk
-  const int64_t k0 = chunk * 16;
+  const int64_t k0 = ((int64_t)blockIdx.x * 64 + threadIdx.x) * kChannelsPerLane;
   if (k0 >= K) return;
-  float zr[16], ir[16];
+  float zr[kChannelsPerLane], ir[kChannelsPerLane];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
+  for (int i = 0; i < kChannelsPerLane / 4; ++i) {
     const float4 zz = reinterpret_cast<const float4 *>(z + k0)[i];
     const float4 ii = reinterpret_cast<const float4 *>(inv_s + k0)[i];
     zr[4 * i + 0] = zz.x; zr[4 * i + 1] = zz.y; zr[4 * i + 2] = zz.z; zr[4 * i + 3] = zz.w;
     ir[4 * i + 0] = ii.x; ir[4 * i + 1] = ii.y; ir[4 * i + 2] = ii.z; ir[4 * i + 3] = ii.w;
   }
-  const int64_t row_step = (int64_t)gridDim.y * kWavesPerBlock;
-  for (int64_t r = (int64_t)blockIdx.y * kWavesPerBlock + threadIdx.y; r < M;
-       r += row_step) {
-    const uint4 *src = reinterpret_cast<const uint4 *>(x + r * K + k0);
-    const uint4 lo = src[0], hi = src[1];
-    const uint32_t words[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
-    int q[16];
+  // groups of kRowsPerWave consecutive rows, one per wave at a time
+  const int64_t group_step = (int64_t)gridDim.y * kWavesPerBlock;
+  for (int64_t g = (int64_t)blockIdx.y * kWavesPerBlock + threadIdx.y; g * kRowsPerWave < M;
+       g += group_step) {
+    const int64_t r0 = g * kRowsPerWave;
+    uint4 v[kRowsPerWave];
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      const uint16_t h = (uint16_t)(words[i >> 1] >> (16 * (i & 1)));
-      const float t = half_bits_to_float(h) - zr[i];  // fp32, RNE
-      const float u = t * ir[i];                      // fp32, RNE
-      q[i] = (int)rintf(fminf(fmaxf(u, -qa), qa));
+    for (int u = 0; u < kRowsPerWave; ++u)
+      v[u] = r0 + u < M ? *reinterpret_cast<const uint4 *>(x + (r0 + u) * K + k0)
+                        : make_uint4(0, 0, 0, 0);
+#pragma unroll
+    for (int u = 0; u < kRowsPerWave; ++u) {
+      if (r0 + u >= M) break;
+      const uint32_t words[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
+      int q[kChannelsPerLane];
+#pragma unroll
+      for (int i = 0; i < kChannelsPerLane; ++i) {
+        const uint16_t h = (uint16_t)(words[i >> 1] >> (16 * (i & 1)));
+        const float t = half_bits_to_float(h) - zr[i];  // fp32, RNE
+        const float w = t * ir[i];                      // fp32, RNE
+        q[i] = (int)rintf(fminf(fmaxf(w, -qa), qa));
+      }
+      *reinterpret_cast<uint2 *>(Xq + (r0 + u) * K + k0) =
+          make_uint2(pack4(q[0], q[1], q[2], q[3]), pack4(q[4], q[5], q[6], q[7]));
     }
-    uint4 out;
-    out.x = pack4(q[0], q[1], q[2], q[3]);
-    out.y = pack4(q[4], q[5], q[6], q[7]);
-    out.z = pack4(q[8], q[9], q[10], q[11]);
-    out.w = pack4(q[12], q[13], q[14], q[15]);
-    *reinterpret_cast<uint4 *>(Xq + r * K + k0) = out;
   }
 }
 
@@ -133,7 +141,7 @@ using namespace detail;
 
 hipError_t launch_quantize_act(const uint16_t *x, int64_t M, int64_t K, int qa, const float *z,
                                const float *inv_s, int8_t *Xq, hipStream_t st) {
-  const int64_t chunks = K / 16;
+  const int64_t chunks = K / kChannelsPerLane;
   const unsigned gx = (unsigned)((chunks + 63) / 64);
   int64_t gy = (M + (int64_t)kWavesPerBlock * kRowsPerWave - 1) /
                ((int64_t)kWavesPerBlock * kRowsPerWave);

@@ -129,6 +129,20 @@ def test_quantize_act_parity(M, K, a_bits):
     assert np.array_equal(got, O.quantize_act(x, z, inv_s, a_bits))
 
 
+def test_quantize_act_rows_beyond_one_grid():
+    # more rows than one launch grid covers (65535 x 16 row groups of 4 rows
+    # per wave, 4 waves per workgroup): the waves loop over further groups,
+    # and the last group is ragged
+    M, K = 65535 * 16 + 37, 32
+    r = np.random.default_rng(11)
+    x = (r.standard_normal((M, K)) * 3).astype(np.float16)
+    z = r.uniform(-1, 1, size=K).astype(np.float32)
+    inv_s = r.uniform(2, 20, size=K).astype(np.float32)
+    case(f"quantize grid-stride M={M} K={K}")
+    got = host(ot.quantize_act(dev(x), 8, dev(z), dev(inv_s)))
+    assert np.array_equal(got, O.quantize_act(x, z, inv_s, 8))
+
+
 def test_quantize_act_ties_and_clamps():
     v = np.array([2.5, 3.5, -2.5, -0.5, 0.5, 1.5, 200.0, -200.0, 126.5, -127.5, 0.0, -0.0,
                   65504, -65504, 1e-7, 6.5], dtype=np.float16)
@@ -170,9 +184,11 @@ QL_SHAPES = [
     (24, 32768, 160), (40, 32769, 64), (64, 33000, 272), (18, 40003, 48),
     (48, 20000, 1040), (30, 20000, 528), (64, 24576, 272), (17, 24577, 1040),
     (40, 30000, 1040),
-    # prefill kernel
+    # prefill kernel; half the tiles (a checkerboard) walk K from its second
+    # 128-byte tile and wrap round: grids with such tiles at one K tile
+    # (K = 48, 128) and at two with a ragged tail (K = 144)
     (65, 256, 128), (200, 300, 400), (256, 256, 256), (300, 772, 1040), (513, 129, 768),
-    (600, 1024, 4112),
+    (600, 1024, 4112), (300, 772, 48), (257, 600, 128), (520, 700, 144),
 ]
 
 
