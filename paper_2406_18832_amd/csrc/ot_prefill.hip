@@ -437,15 +437,16 @@ using namespace detail;
 
 // Relative time of a launch with BN x BM tiles, one workgroup per CU: whole
 // passes over the CUs, each as long as one tile.  A tile's time is
-// proportional to its products (the matrix cores run power-limited, so the
-// wider tile is no cheaper per product) over K plus its epilogue, which
-// costs about as much as 820 more K steps (measured on MI355X).  Penalties:
-// 2 % for the wider tile, so that ties keep 256 x 256; 1.5 for the shorter
-// tile, which stages 1.5 times the operand bytes per product.
+// proportional to its products over K plus its epilogue, which costs about
+// as much as 820 more K steps, times a factor per tile shape for the operand
+// bytes it stages per product: 0.97 for the wider tile (fewer bytes per
+// product), 1.5 for the shorter one (1.5 times the bytes).  Measured on
+// MI355X, per pass against 256 x 256 at the OPT-6.7B, -13B and -66B layer
+// shapes: 0.93-1.01 and 1.3-1.6.
 static double prefill_cost(int64_t M, int64_t N, int64_t K, int bn, int bm, int cus) {
   const int64_t tiles = ((M + bm - 1) / bm) * ((N + bn - 1) / bn);
   const int64_t passes = (tiles + cus - 1) / cus;
-  const double penalty = bn == 320 ? 1.02 : bm == 128 ? 1.5 : 1.0;
+  const double penalty = bn == 320 ? 0.97 : bm == 128 ? 1.5 : 1.0;
   return (double)passes * bn * bm * ((double)K + 820.0) * penalty;
 }
 

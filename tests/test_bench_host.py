@@ -12,7 +12,7 @@ import bench
 
 # OPT-13B W6A6 step, 4096 tokens: (layer, channels N, K, tile channels x tokens)
 OPT13B = [("qkv", 15360, 5120, 320, 256), ("out", 5120, 5120, 320, 256),
-          ("fc1", 20480, 5120, 256, 256), ("fc2", 5120, 20480, 320, 256)]
+          ("fc1", 20480, 5120, 320, 256), ("fc2", 5120, 20480, 320, 256)]
 
 
 @pytest.mark.parametrize("name,N,K,bn,bm", OPT13B)
