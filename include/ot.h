@@ -144,15 +144,20 @@ ot_status ot_quantize_act(const uint16_t *x, int64_t M, int64_t K, int a_bits,
  * ot_ln_quantize_act -- LayerNorm fused with symmetrization and Eq. (g)'s
  * per-channel quantization (Sec. 3.2: z is taken into the LayerNorm's bias,
  * Implementation paragraph: the quantization is fused with the LayerNorm
- * that precedes the linear).  Per row of h:
- *   mean = sum_k h_k / K,  var = sum_k (h_k - mean)^2 / K   (float64)
- *   rstd = 1 / sqrt(var + eps)                              (float64)
+ * that precedes the linear).  Per row of h, with a_k = h_k 2^24 (an exact
+ * integer for every fp16 value), S1 = sum_k a_k and S2 = sum_k a_k^2
+ * (exact integers) and each float64 step rounded to nearest:
+ *   mean = fl(fl(S1) / K) 2^-24
+ *   var  = fl(fl(K S2 - S1^2) / K^2) 2^-48       (population variance)
+ *   rstd = fl(1 / fl(sqrt(fl(var + eps))))
  * and per element, in fp32 rounded to nearest even (no fused multiply-add):
  *   Xq[m,k] = clip(rne((((h - fp32(mean)) * fp32(rstd)) * gamma_k
  *                       + (beta_k - z_k)) * inv_s_k), -qa, qa)
- * The float64 sums run in a fixed order, so the codes are the same on every
- * run; fp32(mean) and fp32(rstd) are the fp32 roundings of the exact values
- * unless those lie within a few float64 units of an fp32 rounding boundary.
+ * The codes are exactly these.  The kernel reaches fp32(mean) and
+ * fp32(rstd) through float64 sums with a proven error bound, and through
+ * the exact integer sums for the rows that bound cannot settle (a mean or
+ * rstd within the bound of an fp32 rounding boundary, e.g. a mean of 0), so
+ * such rows cost more.
  * The normalized fp16 activation is never written.
  *
  *   h      [M x K] fp16 LayerNorm input (device).  M >= 0 (0 is a no-op),
@@ -293,6 +298,22 @@ ot_status ot_qlinear_per_token(const int8_t *Xq, const int8_t *Wq,
  * current device (0 if none; also 0 for sizes the calls reject).
  * Synchronous, no device work. */
 size_t ot_qlinear_workspace_size(int64_t M, int64_t N, int64_t K);
+
+/*
+ * ot_qlinear_plan -- which kernel configuration the quantized-linear calls
+ * (ot_qlinear and its per-token and asymmetric variants, or, with
+ * packed != 0, ot_qlinear_packed) launch for these sizes on the current
+ * device, given a workspace (with_workspace != 0) or not.  Writes a
+ * NUL-terminated description into buf (at most len bytes, truncated if
+ * longer): "none" for M == 0; "prefill 256x256", "prefill 320x256" or
+ * "prefill 256x128" (output channels x tokens per workgroup) above 64
+ * tokens; "decode <layout> <R>-row tiles", with " split-K <runs>" where K
+ * is split, up to 64 tokens.  OT_EINVAL for a NULL buf or len 0, OT_ESHAPE
+ * for sizes the calls reject.  Synchronous, no device work; for
+ * introspection and tests (the results never depend on the plan).
+ */
+ot_status ot_qlinear_plan(int64_t M, int64_t N, int64_t K, int packed,
+                          int with_workspace, char *buf, size_t len);
 
 /*
  * Packed weights for decode.  The folded codes (Eq. (f) right-hand side,

@@ -2,6 +2,7 @@
 // then kernel launches on the caller's stream.  Nothing here allocates
 // device memory or keeps state between calls.
 #include <math.h>
+#include <stdio.h>
 #include <string.h>
 
 #include <vector>
@@ -258,6 +259,21 @@ ot_status ot_qlinear_packed(const int8_t *Xq, const int8_t *Wp, const float *sW,
   return hip_status(ot::launch_qgemm_decode(Xq, Wp, nullptr, nullptr, sW, bprime, M, N, K, Y,
                                             acc_out, workspace, true,
                                             static_cast<hipStream_t>(stream)));
+}
+
+ot_status ot_qlinear_plan(int64_t M, int64_t N, int64_t K, int packed, int with_workspace,
+                          char *buf, size_t len) {
+  if (!buf || len == 0 || M < 0 || N < 0 || K < 0) return OT_EINVAL;
+  if (N == 0 || K < 16 || K % 16 != 0 || K > kMaxK || M > kMaxRows || N > kMaxRows ||
+      !grid_ok(M, N) || (packed && M > 64))
+    return OT_ESHAPE;
+  if (M == 0)
+    snprintf(buf, len, "none");
+  else if (M <= 64)
+    ot::describe_decode(M, N, K, packed != 0, with_workspace != 0, buf, len);
+  else
+    snprintf(buf, len, "%s", ot::prefill_tile_name(M, N, K));
+  return OT_OK;
 }
 
 size_t ot_qlinear_workspace_size(int64_t M, int64_t N, int64_t K) {

@@ -64,6 +64,11 @@ hipError_t launch_pack_weights(const int8_t *Wq, int64_t N, int64_t K, int8_t *W
                                hipStream_t st);
 // Scratch bytes the decode kernels use for split-K partial sums (0: none).
 size_t qgemm_decode_workspace_bytes(int64_t M, int64_t N, int64_t K);
+// The prefill tile launch_qgemm_prefill picks ("prefill 320x256", ...).
+const char *prefill_tile_name(int64_t M, int64_t N, int64_t K);
+// The decode configuration launch_qgemm_decode picks, as text.
+void describe_decode(int64_t M, int64_t N, int64_t K, bool packed, bool workspace, char *buf,
+                     size_t len);
 hipError_t launch_qgemm_prefill(const int8_t *Xq, const int8_t *Wq, const float *sX,
                                 const int32_t *zW, const float *sW, const float *bprime,
                                 int64_t M, int64_t N, int64_t K, uint16_t *Y, int32_t *acc_out,

@@ -2,6 +2,8 @@
 // streaming the weights from HBM.
 #include <algorithm>
 
+#include <stdio.h>
+
 #include "ot_gemm_common.h"
 
 namespace ot {
@@ -706,6 +708,22 @@ static hipError_t decode_tiles(const DecodePlan &p, const int8_t *Xq, const int8
   if (p.rows == 96) OT_TILE(4, 2, 4, 3, 256, 3);
   OT_TILE(4, 8, 1, 1, 128, 4);
 #undef OT_TILE
+}
+
+void describe_decode(int64_t M, int64_t N, int64_t K, bool packed, bool workspace, char *buf,
+                     size_t len) {
+  const int64_t cus = device_cus();
+  const char *layout = packed ? "packed" : "row-major";
+  if (M <= 16) {
+    const int rows = N <= 16 * cus ? 16 : (packed && N > 32 * cus && N <= 64 * cus) ? 64 : 32;
+    snprintf(buf, len, "decode %s %d-row tiles", layout, rows);
+    return;
+  }
+  const DecodePlan p = decode_plan(M, N, K, cus, workspace);
+  if (p.runs > 1)
+    snprintf(buf, len, "decode %s %d-row tiles split-K %d", layout, p.rows, p.runs);
+  else
+    snprintf(buf, len, "decode %s %d-row tiles", layout, p.rows);
 }
 
 // Wq: the weight codes [N x K], or (packed) their micro-tiles.

@@ -3,21 +3,30 @@
 // the quantization of Eq. (g) is fused with the LayerNorm that precedes the
 // linear, so the fp16 activation never goes to memory).
 //
-// Per row h [K] (fp16), with c = h_0 and d_k = h_k - c (exact in float64):
-//   mean = c + sum_k d_k / K                            float64
-//   var  = sum_k d_k^2 / K - (sum_k d_k / K)^2          (population variance)
-//   rstd = 1 / sqrt(var + eps)                          float64
+// Row statistics, exactly as defined: every fp16 value is an integer
+// multiple of 2^-24, so a_k = h_k 2^24 is an integer (|a_k| < 2^40) and the
+// sums S1 = sum a_k and S2 = sum a_k^2 are exact integers.  Then, each step
+// rounded to nearest in float64,
+//   mean = fl(fl(S1) / K) 2^-24
+//   var  = fl(fl(K S2 - S1^2) / K^2) 2^-48          (population variance)
+//   rstd = fl(1 / fl(sqrt(fl(var + eps))))
 //   mu32 = fp32(mean), r32 = fp32(rstd)
 // and per element (fp32 operations, round to nearest even, no contraction):
 //   y = ((fp32(h_k) - mu32) * r32) * gamma_k + (beta_k - z_k)
 //   q = clip(rne(y * inv_s_k), -qa, qa)
 //
-// The float64 sums run in a fixed order (each thread's chunks in order, a
-// fixed butterfly across a wave, waves in order), so the result does not
-// change from run to run.  Their relative error, a few units of the 53rd
-// bit (times (mean - c)^2 / var for the variance), is far below fp32's 24
-// bits: mu32 and r32 are the fp32 roundings of the exact mean and rstd
-// except when those lie that close to an fp32 rounding boundary.
+// Two ways to the same mu32 and r32.  The fast one sums d_k = h_k - c with
+// c = h_0 (exact in float64) in float64, in a fixed order (each thread's
+// chunks, a butterfly across a wave, waves in order), and bounds its own
+// error: a sum whose terms pass through at most n additions is off by at
+// most n 2^-53 times the sum of their magnitudes (and sum |d_k| <=
+// sqrt(K sum d_k^2)).  If the float64 mean and rstd lie farther than that
+// bound (plus the rounding error of the exact procedure itself) from every
+// fp32 rounding boundary, their fp32 roundings are the exact ones.  Rows
+// where they do not (rare: a few in 10^5 on spread-out rows; always for a
+// row whose mean is 0 but whose values are not all 0) take the second way:
+// exact integer sums (S1 in 64 bits, S2 in 128 bits) and the float64 steps
+// above.  Both paths give the same codes on every run.
 //
 // HBM-bound: 2 bytes in, 1 byte out per element.  A workgroup of T threads
 // takes R rows; thread t owns the 8-channel chunks t, t + T, ... (CPT of
@@ -36,6 +45,58 @@ __device__ inline float half_hi(uint32_t w) { return half_bits_to_float((uint16_
 __device__ inline double wave_sum(double v) {
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off);
+  return v;
+}
+
+// h 2^24 as an exact integer (|.| < 2^40): (1024 + m) 2^(e - 1) for a
+// normal fp16 with exponent field e and mantissa field m, m for a subnormal.
+__device__ inline int64_t half_fixed24(uint32_t b) {
+  const int e = (b >> 10) & 31;
+  const int64_t m = b & 1023;
+  const int64_t mag = e ? (m + 1024) << (e - 1) : m;
+  return (b & 0x8000u) ? -mag : mag;
+}
+
+typedef unsigned __int128 u128;
+
+// Nearest float64 to a 128-bit unsigned integer (ties to even).
+__device__ inline double u128_to_double(u128 v) {
+  const uint64_t hi = (uint64_t)(v >> 64);
+  if (hi == 0) return (double)(uint64_t)v;  // one correctly rounded conversion
+  const int lz = __builtin_clzll(hi);
+  const u128 n = v << lz;                   // leading one at bit 127
+  const uint64_t top = (uint64_t)(n >> 64);
+  const bool sticky = (uint64_t)n != 0;
+  uint64_t mant = top >> 11;                // 53 bits
+  const uint64_t rest = top & 0x7FF;
+  if (rest > 0x400 || (rest == 0x400 && (sticky || (mant & 1)))) ++mant;
+  return ldexp((double)mant, 75 - lz);      // bit 0 of mant has weight 2^(75 - lz)
+}
+
+// True when x and the value it stands for, known to within err, may lie on
+// different sides of a boundary between two fp32 rounding cells, i.e. when
+// fp32(x) is not certain to be the fp32 rounding of that value.
+__device__ inline bool near_fp32_boundary(double x, double err) {
+  const float f = (float)x;
+  if (!isfinite(f) || !(err < 1e300)) return true;
+  const double up = 0.5 * ((double)f + (double)nextafterf(f, INFINITY));
+  const double dn = 0.5 * ((double)f + (double)nextafterf(f, -INFINITY));
+  return x + err >= up || x - err <= dn;
+}
+
+// Wave-wide exact sums (lane 0 ends with the totals).
+__device__ inline int64_t wave_sum_i64(int64_t v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off);
+  return v;
+}
+__device__ inline u128 wave_sum_u128(u128 v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    const uint64_t lo = __shfl_xor((unsigned long long)(uint64_t)v, off);
+    const uint64_t hi = __shfl_xor((unsigned long long)(uint64_t)(v >> 64), off);
+    v += ((u128)hi << 64) | lo;
+  }
   return v;
 }
 
@@ -94,7 +155,13 @@ __global__ __launch_bounds__(MAXT) void ln_quantize_kernel(
     }
   }
   __syncthreads();
+  // No term of the float64 sums passes through more than this many
+  // additions: 8 per chunk in a thread, 6 butterfly levels, one per wave.
+  const double kU = 0x1p-53;
+  const double gam = 1.01 * kU * (double)(8 * CPT + 6 + nwaves + 2);
   float mu32[R], r32[R];
+  bool exact[R];
+  bool any_exact = false;
 #pragma unroll
   for (int r = 0; r < R; ++r) {
     double s1 = 0.0, s2 = 0.0;
@@ -103,9 +170,75 @@ __global__ __launch_bounds__(MAXT) void ln_quantize_kernel(
       s2 += red[1][w][r];
     }
     const double dm = s1 / (double)K;  // mean - c
+    const double mean = cs[r] + dm;
     const double var = fmax(s2 / (double)K - dm * dm, 0.0);
-    mu32[r] = (float)(cs[r] + dm);
-    r32[r] = (float)(1.0 / sqrt(var + eps));
+    const double ve = var + eps;
+    const double rstd = 1.0 / sqrt(ve);
+    mu32[r] = (float)mean;
+    r32[r] = (float)rstd;
+    // error bounds against the exact procedure (its own roundings included)
+    const double rms = sqrt(s2 / (double)K) * (1.0 + 1e-9);   // >= sum |d_k| / K
+    const double e_dm = gam * rms + kU * fabs(dm);
+    const double e_mean = 1.1 * (e_dm + 4.0 * kU * fabs(mean));
+    const double e_var = 1.1 * ((gam + 2.0 * kU) * rms * rms + (2.0 * fabs(dm) + 2.0 * e_dm) * e_dm +
+                                kU * dm * dm + 4.0 * kU * var);
+    const double e_rstd = rstd * (0.55 * (e_var + 3.0 * kU * ve) / ve + 6.0 * kU);
+    exact[r] = row0 + r < M &&
+               (near_fp32_boundary(mean, e_mean) || near_fp32_boundary(rstd, e_rstd));
+    any_exact |= exact[r];
+  }
+
+  // the exact procedure for the rows the bound cannot settle (every thread
+  // takes the same branch: the values above are identical in all of them)
+  if (any_exact) {
+    __shared__ int64_t xs1[16][R];
+    __shared__ uint64_t xs2[2][16][R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      if (!exact[r]) continue;
+      // re-read from the L2 rather than from the registers that hold the
+      // row: this branch then adds little to the kernel's register budget
+      int64_t e1 = 0;
+      u128 e2 = 0;
+      const uint16_t *hr = h + (row0 + r) * K;
+#pragma unroll 1
+      for (int ch = t; ch < nchunks; ch += T) {
+        const uint4 v = *reinterpret_cast<const uint4 *>(hr + (int64_t)ch * 8);
+        const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          const int64_t a = half_fixed24((i & 1) ? (w[i >> 1] >> 16) : (w[i >> 1] & 0xFFFFu));
+          const uint64_t m = (uint64_t)(a < 0 ? -a : a);
+          e1 += a;
+          e2 += (u128)m * m;
+        }
+      }
+      e1 = wave_sum_i64(e1);
+      e2 = wave_sum_u128(e2);
+      if (lane == 0) {
+        xs1[wave][r] = e1;
+        xs2[0][wave][r] = (uint64_t)e2;
+        xs2[1][wave][r] = (uint64_t)(e2 >> 64);
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      if (!exact[r]) continue;
+      int64_t S1 = 0;
+      u128 S2 = 0;
+      for (int w = 0; w < nwaves; ++w) {
+        S1 += xs1[w][r];
+        S2 += ((u128)xs2[1][w][r] << 64) | xs2[0][w][r];
+      }
+      const uint64_t m1 = (uint64_t)(S1 < 0 ? -S1 : S1);
+      const u128 D = (u128)(uint64_t)K * S2 - (u128)m1 * m1;  // K^2 var 2^48 >= 0
+      const double mean = ((double)S1 / (double)K) * 0x1p-24;
+      const double var = (u128_to_double(D) / ((double)K * (double)K)) * 0x1p-48;
+      const double rstd = 1.0 / sqrt(var + eps);
+      mu32[r] = (float)mean;
+      r32[r] = (float)rstd;
+    }
   }
 
   // normalize, shifted affine, quantize; each chunk's gamma,

@@ -473,6 +473,14 @@ static PrefillTile prefill_tile(int64_t M, int64_t N, int64_t K) {
   return PrefillTile::k256x256;
 }
 
+const char *prefill_tile_name(int64_t M, int64_t N, int64_t K) {
+  switch (prefill_tile(M, N, K)) {
+    case PrefillTile::k320x256: return "prefill 320x256";
+    case PrefillTile::k256x128: return "prefill 256x128";
+    default: return "prefill 256x256";
+  }
+}
+
 hipError_t launch_qgemm_prefill(const int8_t *Xq, const int8_t *Wq, const float *sX,
                                 const int32_t *zW, const float *sW, const float *bprime,
                                 int64_t M, int64_t N, int64_t K, uint16_t *Y, int32_t *acc_out,

@@ -71,6 +71,8 @@ def lib() -> ctypes.CDLL:
         L.ot_qlinear.argtypes = [vp, vp, vp, vp, i64, i64, i64, c_int, c_int, vp, vp, vp, vp]
         L.ot_qlinear_workspace_size.restype = ctypes.c_size_t
         L.ot_qlinear_workspace_size.argtypes = [i64, i64, i64]
+        L.ot_qlinear_plan.restype = c_int
+        L.ot_qlinear_plan.argtypes = [i64, i64, i64, c_int, c_int, ctypes.c_char_p, ctypes.c_size_t]
         L.ot_packed_weights_size.restype = ctypes.c_size_t
         L.ot_packed_weights_size.argtypes = [i64, i64]
         L.ot_pack_weights.restype = c_int
@@ -211,6 +213,15 @@ def ot_qlinear(Xq, Wq, sW, bprime, a_bits, w_bits, Y, acc_out=None, workspace=No
 
 def ot_qlinear_workspace_size(M: int, N: int, K: int) -> int:
     return int(lib().ot_qlinear_workspace_size(M, N, K))
+
+
+def ot_qlinear_plan(M: int, N: int, K: int, packed=False, with_workspace=False) -> str:
+    """The kernel configuration the quantized-linear calls launch for these
+    sizes on the current device (text; no device work)."""
+    buf = ctypes.create_string_buffer(96)
+    _check(lib().ot_qlinear_plan(M, N, K, int(bool(packed)), int(bool(with_workspace)), buf,
+                                 len(buf)), "ot_qlinear_plan")
+    return buf.value.decode()
 
 
 def ot_packed_weights_size(N: int, K: int) -> int:

@@ -1,14 +1,14 @@
 """GPU parity of ot_ln_quantize_act (LayerNorm fused with symmetrization and
 per-channel quantization, Sec. 3.2) against the CPU oracle, through the C
-ABI.
+ABI: codes bit for bit.
 
-The oracle takes the row statistics exactly; the kernel sums in float64 in a
-fixed order, so its fp32 mean and rstd can differ from the oracle's by one
-fp32 unit when the exact value lies within a few float64 units of an fp32
-rounding boundary.  Codes are therefore compared bit for bit everywhere
-except inside the window of a rounding tie that such a one-unit change can
-move a value across; there they may differ by one.  (No test case here has
-hit that window so far; the check exists so that the bar is stated.)"""
+The kernel takes the row statistics on a float64 fast path with a proven
+error bound and falls back to exact integer sums for the rows the bound
+cannot settle; the oracle takes them exactly.  Besides random and workload
+rows, the cases below build rows that must take the fallback (a mean of
+exactly 0, a mean exactly halfway between two fp32 values) and give each
+row a channel where a one-unit change of fp32(mean) or fp32(rstd) moves the
+code by about 20, so a wrong rounding cannot hide."""
 import numpy as np
 import pytest
 import torch
@@ -51,24 +51,11 @@ def _random_inputs(M, K, seed, a_bits=8, eps=1e-5):
 
 
 def assert_codes_match(got, H, gamma, beta, eps, z, inv_s, a_bits):
-    qa = O.qmax(a_bits)
-    u = O.ln_scaled_act(H, gamma, beta, eps, z, inv_s).astype(np.float64)
-    ref = np.clip(np.rint(u), -qa, qa)
-    differ = got.astype(np.float64) != ref
-    if not differ.any():
-        return
-    mean, var = O.layernorm_stats(H)
-    mu32 = np.abs(mean.astype(np.float32).astype(np.float64))[:, None]
-    r32 = (1.0 / np.sqrt(var + float(np.float32(eps))))[:, None]
-    g = np.abs(gamma.astype(np.float64))[None, :]
-    i = np.abs(inv_s.astype(np.float64))[None, :]
-    c = np.abs(beta.astype(np.float64) - z.astype(np.float64))[None, :]
-    # a one-unit change of fp32(mean) or fp32(rstd), and the fp32 roundings
-    # after it, move u by at most this much
-    window = 2.0 ** -23 * (2 * mu32 * r32 * g * i + 8 * (np.abs(u) + c * i)) + 2.0 ** -20
-    near_tie = np.abs(np.abs(u - np.trunc(u)) - 0.5) <= window
-    assert np.all(np.abs(got[differ].astype(int) - ref[differ]) <= 1)
-    assert np.all(near_tie[differ]), f"{int((differ & ~near_tie).sum())} codes differ away from a tie"
+    ref = O.ln_quantize_act(H, gamma, beta, eps, z, inv_s, a_bits)
+    assert got.shape == ref.shape
+    differ = got != ref
+    assert not differ.any(), (f"{int(differ.sum())} of {differ.size} codes differ, rows "
+                              f"{np.unique(np.nonzero(differ)[0])[:10]}")
 
 
 def _run(H, gamma, beta, eps, a_bits, z, inv_s):
@@ -150,9 +137,9 @@ def test_parity_workload_inputs(name, li):
     assert_codes_match(got, H, gamma, beta, 1e-5, z, inv_s, wl.a_bits)
 
 
-def test_fullsize_opt13b_qkv_input_sampled_rows():
-    """4096 x 5120 (the OPT-13B qkv input): every code in range, sampled rows
-    against the oracle, and the run repeated gives identical bytes."""
+def test_fullsize_opt13b_qkv_input_every_row():
+    """4096 x 5120 (the OPT-13B qkv input): every code against the oracle,
+    and the run repeated gives identical bytes."""
     wl = synth.WORKLOADS["opt13b_w6a6"]
     K, M = wl.layers[0].K, wl.M
     case(f"ln_quantize fullsize M={M} K={K}")
@@ -165,11 +152,109 @@ def test_fullsize_opt13b_qkv_input_sampled_rows():
     Xq2 = ot.ln_quantize_act(*args)
     torch.cuda.synchronize()
     assert torch.equal(Xq, Xq2)
-    assert int(Xq.abs().max()) <= O.qmax(wl.a_bits)
-    rows = np.array(sorted(set(np.random.default_rng(1).choice(M, 48, replace=False).tolist())
-                           | {0, M - 1}))
-    got = Xq.index_select(0, torch.from_numpy(rows).cuda()).cpu().numpy()
-    assert_codes_match(got, H[rows], gamma, beta, 1e-5, z, inv_s, wl.a_bits)
+    got = Xq.cpu().numpy()
+    assert int(np.abs(got).max()) <= O.qmax(wl.a_bits)
+    assert_codes_match(got, H, gamma, beta, 1e-5, z, inv_s, wl.a_bits)
+
+
+def _sensitive(H, gamma, beta, z, inv_s, eps):
+    """Gives row m its own channel j = 1 + m where the code moves by about 20
+    if fp32(mean) or fp32(rstd) of that row is off by one unit: a gain of
+    65504, a reciprocal scale of 1e4, and a shift that brings the row's
+    value there near 0.  Uses the oracle's statistics (test input only)."""
+    gamma, beta, z, inv_s = gamma.copy(), beta.copy(), z.copy(), inv_s.copy()
+    mean, var = O.layernorm_stats(H)
+    mu32 = mean.astype(np.float32)
+    r32 = (1.0 / np.sqrt(var + float(np.float32(eps)))).astype(np.float32)
+    for m in range(H.shape[0]):
+        j = 1 + m
+        gamma[j] = np.float16(65504.0)
+        beta[j] = np.float16(0.0)
+        inv_s[j] = np.float32(1e4)
+        g = ((H[m, j].astype(np.float32) - mu32[m]) * r32[m]) * np.float32(65504.0)
+        z[j] = np.float32(g) + np.float32(3e-4)
+    return gamma, beta, z, inv_s
+
+
+def _zero_mean_rows(r, M, K):
+    """Rows whose values cancel in pairs: the mean is exactly 0, the spread
+    is not, so the float64 bound can never settle fp32(mean)."""
+    rows = []
+    for i in range(M):
+        half = (r.standard_normal(K // 2) * r.uniform(0.05, 30.0)).astype(np.float16)
+        row = np.concatenate([half, -half])
+        r.shuffle(row)
+        rows.append(row)
+    return np.stack(rows).astype(np.float16)
+
+
+def _tie_mean_rows(r, M, K, first_channel):
+    """Rows whose exact mean lies halfway between two adjacent fp32 values,
+    tuned with one subnormal element (a step of 2^-24 in the row sum).  Row
+    i holds a value near its mean at channel first_channel + i, where a
+    one-unit change of fp32(mean) then changes h - mean exactly."""
+    from fractions import Fraction
+    rows = []
+    while len(rows) < M:
+        off = r.uniform(0.26, 0.49)
+        row = (r.standard_normal(K) + off).astype(np.float16)
+        row[first_channel + len(rows)] = np.float16(off)
+        row[-1] = 0
+        a = row.astype(np.float64) * 2.0 ** 24
+        S = int(a.astype(np.int64).sum())
+        m0 = Fraction(S, K * 2 ** 24)
+        f = np.float32(float(m0))
+        up = np.nextafter(f, np.float32(np.inf))
+        dn = np.nextafter(f, np.float32(-np.inf))
+        mid = min((Fraction(float(f)) + Fraction(float(up))) / 2,
+                  (Fraction(float(f)) + Fraction(float(dn))) / 2, key=lambda v: abs(v - m0))
+        need = mid * K * 2 ** 24 - S
+        if need.denominator != 1 or abs(need) > 1023:
+            continue
+        row[-1] = np.float16(int(need) * 2.0 ** -24)
+        assert Fraction(int((row.astype(np.float64) * 2.0 ** 24).astype(np.int64).sum()),
+                        K * 2 ** 24) == mid
+        rows.append(row)
+    return np.stack(rows).astype(np.float16)
+
+
+@pytest.mark.parametrize("K", [1024, 5120])
+def test_exact_fallback_rows(K):
+    """Rows the float64 bound cannot settle, mixed with ordinary rows, each
+    with a channel that exposes a one-unit error of fp32(mean) or
+    fp32(rstd)."""
+    case(f"ln_quantize exact-fallback rows K={K}")
+    r = np.random.default_rng(K)
+    H = np.concatenate([_zero_mean_rows(r, 12, K), _tie_mean_rows(r, 12, K, 13),
+                        (r.standard_normal((12, K)) * 3 + 0.4).astype(np.float16)])
+    gamma = r.uniform(0.5, 1.5, K).astype(np.float16)
+    beta = r.normal(0, 0.5, K).astype(np.float16)
+    z = r.normal(0, 0.3, K).astype(np.float32)
+    inv_s = r.uniform(10, 40, K).astype(np.float32)
+    for eps in (1e-5, 0.0):
+        g2, b2, z2, i2 = _sensitive(H, gamma, beta, z, inv_s, eps)
+        got = _run(H, g2, b2, eps, 8, z2, i2)
+        assert_codes_match(got, H, g2, b2, eps, z2, i2, 8)
+        # the sensitive channels are in range, so they do test the rounding
+        u = O.ln_scaled_act(H, g2, b2, eps, z2, i2)
+        idx = np.arange(H.shape[0])
+        assert np.all(np.abs(u[idx, 1 + idx]) < 100)
+
+
+@pytest.mark.parametrize("name,li", [("opt13b_w6a6", 2), ("opt66b_w8a8", 0)])
+def test_workload_rows_sensitive(name, li):
+    """Workload LayerNorm inputs (the fast path nearly always) with the
+    sensitive channels."""
+    wl = synth.WORKLOADS[name]
+    K = wl.layers[li].K
+    case(f"ln_quantize sensitive {name}/{wl.layers[li].name} K={K}")
+    gamma, beta = synth.ln_params(wl, li)
+    calib = [_textbook_ln_fp16(synth.ln_inputs(wl, li, 128, 1), gamma, beta, 1e-5)]
+    _, z, s, inv_s = O.calibrate(calib, 8)
+    H = synth.ln_inputs(wl, li, 64)
+    g2, b2, z2, i2 = _sensitive(H, gamma, beta, z, inv_s, 1e-5)
+    got = _run(H, g2, b2, 1e-5, 8, z2, i2)
+    assert_codes_match(got, H, g2, b2, 1e-5, z2, i2, 8)
 
 
 def test_close_to_unfused_layernorm_then_quantize():

@@ -278,6 +278,18 @@ def test_pipeline_opt125m(a_bits, w_bits):
 # ragged M, N and K.
 # --------------------------------------------------------------------------
 PREFILL_TILE_SHAPES = [(500, 40860, 272), (300, 1000, 1040), (2000, 5000, 272)]
+PREFILL_TILE_ON_256_CUS = {(500, 40860, 272): "prefill 320x256", (300, 1000, 1040): "prefill 256x128",
+                           (2000, 5000, 272): "prefill 256x256"}
+
+
+def test_prefill_tiles_all_covered():
+    """The tile shapes above are the ones the library runs (on a 256-CU
+    MI355X), so each of the three tiles stays covered."""
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    if cus != 256:
+        pytest.skip(f"tile choice depends on the CU count ({cus} here, 256 on MI355X)")
+    for shape, name in PREFILL_TILE_ON_256_CUS.items():
+        assert ot.ot_qlinear_plan(*shape) == name, shape
 
 
 @pytest.mark.parametrize("M,N,K", PREFILL_TILE_SHAPES)
@@ -286,7 +298,8 @@ def test_prefill_tiles_staged_epilogue(M, N, K, flavour):
     Xq, Wq, sW, bp = _random_qlinear_inputs(M, N, K, 8, 8, M + 3 * N + 7 * K)
     r = np.random.default_rng(N)
     case(f"prefill staged epilogue {flavour} M={M} N={N} K={K} "
-         f"cus={torch.cuda.get_device_properties(0).multi_processor_count}")
+         f"cus={torch.cuda.get_device_properties(0).multi_processor_count} "
+         f"plan={ot.ot_qlinear_plan(M, N, K)}")
     if flavour == "channel":
         Y = ot.qlinear(dev(Xq), dev(Wq), dev(sW), dev(bp), 8, 8)
         ref = O.epilogue(O.int_gemm(Xq, Wq), sW, bp)
