@@ -46,7 +46,9 @@ typedef enum ot_status {
   OT_ESHAPE = 2,     /* K not a multiple of 16, zero-sized where disallowed  */
   OT_ERANGE = 3,     /* K * qa * qw >= 2^31: the int32 accumulator could wrap */
   OT_ENONFINITE = 4, /* NaN or infinity in calibration data or weights       */
-  OT_EHIP = 5        /* a HIP runtime call failed                            */
+  OT_EHIP = 5,       /* a HIP runtime call failed                            */
+  OT_ENOSCRATCH = 6  /* ot_qlinear_noalloc: the sizes need more scratch than  */
+                     /* the library's fixed array holds                      */
 } ot_status;
 
 /* Static, human-readable description of a status code. */
@@ -292,6 +294,29 @@ ot_status ot_qlinear_per_token(const int8_t *Xq, const int8_t *Wq,
                                const float *bprime, int64_t M, int64_t N,
                                int64_t K, int a_bits, int w_bits, uint16_t *Y,
                                int32_t *acc_out, void *workspace, void *stream);
+
+/*
+ * ot_qlinear_noalloc -- ot_qlinear for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc).  Same arguments, checks and results as ot_qlinear
+ * without the workspace argument: where ot_qlinear would use a workspace
+ * (split-K decode, 17..64 tokens), this call uses a fixed device array of
+ * OT_NOALLOC_SCRATCH_BYTES that the library holds on every device it runs
+ * on until the process ends (its address is looked up on the first call on
+ * each device).  It calls no allocation routine.  OT_ENOSCRATCH if
+ * ot_qlinear_workspace_size(M, N, K) exceeds OT_NOALLOC_SCRATCH_BYTES
+ * (then nothing runs; ot_qlinear with a workspace serves such sizes).  On
+ * a 256-CU device that cannot happen: a split plan runs at most one
+ * workgroup per CU, runs x ceil(N / rows) <= 256 with rows <= 128, so it
+ * needs at most 64 x 4 x (32768 + 8) bytes (8.0 MiB).
+ * Calls that overlap in time on one device share the array and race:
+ * serialize them (one stream, or events).  Asynchronous on stream.
+ */
+#define OT_NOALLOC_SCRATCH_BYTES (9u << 20)
+ot_status ot_qlinear_noalloc(const int8_t *Xq, const int8_t *Wq,
+                             const float *sW, const float *bprime, int64_t M,
+                             int64_t N, int64_t K, int a_bits, int w_bits,
+                             uint16_t *Y, int32_t *acc_out, void *stream);
 
 /* Bytes of optional scratch that ot_qlinear, ot_qlinear_per_token,
  * ot_qlinear_asym and ot_qlinear_packed can use for these sizes on the

@@ -44,6 +44,7 @@ const char *ot_strerror(int status) {
     case OT_ERANGE: return "K * qa * qw >= 2^31: the int32 accumulator could overflow";
     case OT_ENONFINITE: return "non-finite value (NaN or infinity) in calibration data or weights";
     case OT_EHIP: return "HIP runtime error";
+    case OT_ENOSCRATCH: return "these sizes need more scratch than ot_qlinear_noalloc's fixed array holds (use ot_qlinear with a workspace)";
     default: return "unknown status";
   }
 }

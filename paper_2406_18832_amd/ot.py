@@ -19,7 +19,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libot.so")
 HEADER = os.path.join(os.path.dirname(HERE), "include", "ot.h")
 
-OT_OK, OT_EINVAL, OT_ESHAPE, OT_ERANGE, OT_ENONFINITE, OT_EHIP = range(6)
+OT_OK, OT_EINVAL, OT_ESHAPE, OT_ERANGE, OT_ENONFINITE, OT_EHIP, OT_ENOSCRATCH = range(7)
 
 _lib = None
 
@@ -69,6 +69,8 @@ def lib() -> ctypes.CDLL:
                                       vp]
         L.ot_qlinear.restype = c_int
         L.ot_qlinear.argtypes = [vp, vp, vp, vp, i64, i64, i64, c_int, c_int, vp, vp, vp, vp]
+        L.ot_qlinear_noalloc.restype = c_int
+        L.ot_qlinear_noalloc.argtypes = [vp, vp, vp, vp, i64, i64, i64, c_int, c_int, vp, vp, vp]
         L.ot_qlinear_workspace_size.restype = ctypes.c_size_t
         L.ot_qlinear_workspace_size.argtypes = [i64, i64, i64]
         L.ot_qlinear_plan.restype = c_int
@@ -209,6 +211,21 @@ def ot_qlinear(Xq, Wq, sW, bprime, a_bits, w_bits, Y, acc_out=None, workspace=No
                           int(w_bits), _dev(Y, torch.float16, "Y", (M, N)),
                           _dev(acc_out, torch.int32, "acc_out", (M, N)), ws, _stream(stream))
     _check(rc, "ot_qlinear")
+
+
+def ot_qlinear_noalloc(Xq, Wq, sW, bprime, a_bits, w_bits, Y, acc_out=None, stream=None):
+    """ot_qlinear with the split-K scratch in the library's fixed device
+    array (no workspace, no allocation).  Asynchronous."""
+    M, K = Xq.shape
+    N = Wq.shape[0]
+    if Wq.shape[1] != K:
+        raise ValueError("Xq and Wq disagree on K")
+    rc = lib().ot_qlinear_noalloc(_dev(Xq, torch.int8, "Xq"), _dev(Wq, torch.int8, "Wq"),
+                                  _dev(sW, torch.float32, "sW", (N,)),
+                                  _dev(bprime, torch.float32, "bprime", (N,)), M, N, K,
+                                  int(a_bits), int(w_bits), _dev(Y, torch.float16, "Y", (M, N)),
+                                  _dev(acc_out, torch.int32, "acc_out", (M, N)), _stream(stream))
+    _check(rc, "ot_qlinear_noalloc")
 
 
 def ot_qlinear_workspace_size(M: int, N: int, K: int) -> int:
