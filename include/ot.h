@@ -17,7 +17,8 @@
  *    transpose.
  *  - Every tensor pointer is a DEVICE pointer owned by the caller.  The
  *    library never allocates, frees or retains caller memory and keeps no
- *    global state; calls on different streams are independent.
+ *    global state (apart from ot_qlinear_noalloc's fixed scratch array);
+ *    calls on different streams are independent.
  *  - fp16 tensors are passed as uint16_t IEEE binary16 bit patterns.
  *  - bits is in [2, 8]; the quantizer is symmetric and signed with largest
  *    code q(bits) = 2^(bits-1) - 1 (127 for 8 bits, 31 for 6 bits).  Codes

@@ -5,6 +5,12 @@ Flags:
                      fused multiply-add would skip one of them.
   -Xclang -target-feature -Xclang -packed-fp32-ops
                      keep the compiler from emitting packed fp32 arithmetic.
+
+build(sanitize=True) builds a copy whose host code (the C ABI's checks,
+launch plans and dispatch) runs under AddressSanitizer and
+UndefinedBehaviorSanitizer; the GPU code is built as usual.  Load it into a
+process with the sanitizer runtime preloaded (asan_runtime() names it) and
+the binding pointed at it (OT_LIBRARY).
 """
 from __future__ import annotations
 
@@ -27,6 +33,14 @@ HIPCC_FLAGS = [
 ]
 
 
+# host side only: each sanitizer flag applies to the host pass alone
+SANITIZE_FLAGS = [
+    "-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+    "-Xarch_host", "-fno-sanitize-recover=undefined", "-Xarch_host", "-fno-omit-frame-pointer",
+    "-g",
+]
+
+
 def hipcc() -> str:
     for cand in (os.environ.get("HIPCC"), "/opt/rocm/bin/hipcc", shutil.which("hipcc")):
         if cand and os.path.exists(cand):
@@ -38,11 +52,30 @@ def sources():
     return sorted(glob.glob(os.path.join(CSRC, "*.hip")))
 
 
-def build(verbose: bool = False, extra_flags=()) -> str:
-    """Compiles every csrc/*.hip into libot.so next to this file and returns
-    its path.  Always recompiles."""
-    tmp = LIB + ".tmp"
-    cmd = [hipcc(), *HIPCC_FLAGS, *extra_flags, *sources(), "-o", tmp]
+def asan_runtime() -> str:
+    """Path of the compiler's AddressSanitizer runtime (to preload into a
+    process that loads the sanitized library)."""
+    clang = os.path.join(os.path.dirname(os.path.realpath(hipcc())), "..", "llvm", "bin", "clang")
+    if not os.path.exists(clang):
+        clang = "/opt/rocm/llvm/bin/clang"
+    out = subprocess.run([clang, "-print-file-name=libclang_rt.asan-x86_64.so"],
+                         capture_output=True, text=True)
+    path = out.stdout.strip()
+    if out.returncode != 0 or not os.path.isabs(path) or not os.path.exists(path):
+        raise RuntimeError("AddressSanitizer runtime not found")
+    return path
+
+
+def build(verbose: bool = False, extra_flags=(), sanitize: bool = False, out: str = None) -> str:
+    """Compiles every csrc/*.hip into libot.so next to this file (or into
+    out) and returns its path.  Always recompiles.  sanitize=True: host code
+    under AddressSanitizer and UndefinedBehaviorSanitizer."""
+    lib = out or LIB
+    tmp = lib + ".tmp"
+    flags = list(HIPCC_FLAGS)
+    if sanitize:
+        flags = [f for f in flags if f != "-O3"] + ["-O1", *SANITIZE_FLAGS]
+    cmd = [hipcc(), *flags, *extra_flags, *sources(), "-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)
@@ -56,8 +89,8 @@ def build(verbose: bool = False, extra_flags=()) -> str:
         if noise not in line and "warning: feature flag" not in line and line.strip():
             if verbose:
                 print(line)
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, lib)
+    return lib
 
 
 if __name__ == "__main__":

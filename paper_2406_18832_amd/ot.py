@@ -4,8 +4,9 @@ Argument marshalling only: torch tensors in, device pointers and the current
 HIP stream out to the library; every computation runs in libot's kernels.
 The names match the C entry points.  Outputs are caller-allocated, as in C.
 
-The library is loaded on first use.  If ``libot.so`` has not been built the
-first call raises: there is no fallback.
+The library is loaded on first use: ``libot.so`` next to this file, or the
+build named by the environment variable OT_LIBRARY (e.g. a sanitizer build).
+If it has not been built the first call raises: there is no fallback.
 """
 from __future__ import annotations
 
@@ -16,7 +17,7 @@ import re
 import torch
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "libot.so")
+LIB_PATH = os.environ.get("OT_LIBRARY") or os.path.join(HERE, "libot.so")
 HEADER = os.path.join(os.path.dirname(HERE), "include", "ot.h")
 
 OT_OK, OT_EINVAL, OT_ESHAPE, OT_ERANGE, OT_ENONFINITE, OT_EHIP, OT_ENOSCRATCH = range(7)
