@@ -18,7 +18,11 @@ packed weights (ot_pack_weights, ot_qlinear_packed); `mixed_block` times the pap
 asymmetric ("Int8") weights; `ln_quantize` times the LayerNorm fused with
 symmetrization and quantization (qkv and fc1 inputs) against torch's
 LayerNorm plus ot_quantize_act; `fp16_baseline` times torch's fp16 linear on
-the same shapes; `cpu_baseline` times the CPU oracle on a bounded sample.
+the same shapes; `cpu_baseline` times the CPU oracle on a bounded sample;
+`other_prefill` times the OPT-6.7B (W8A8, 2048 tokens) and OPT-66B (W8A8,
+8192 tokens) steps the same way, with their fp16 speedup and weight-memory
+ratio, and `paper_context` quotes the paper's own speed and memory figures
+with the hardware it names.
 """
 from __future__ import annotations
 
@@ -54,6 +58,8 @@ def parse():
     p.add_argument("--no-sclk", action="store_true",
                    help="skip the shader-clock window (about 1 s of untimed prefill steps)")
     p.add_argument("--no-ln", action="store_true", help="skip the fused LayerNorm report")
+    p.add_argument("--no-other", action="store_true",
+                   help="skip the OPT-6.7B and OPT-66B prefill reports")
     p.add_argument("--no-asym", action="store_true",
                    help="skip the asymmetric-weight step report")
     p.add_argument("--no-mixed", action="store_true",
@@ -748,6 +754,111 @@ def shader_clock_window(torch, step, seconds=1.0):
             pass
 
 
+def time_prefill_step(torch, ot, wl, layers, steps, warmup):
+    """The timed prefill step: for each linear, ot_quantize_act then
+    ot_qlinear, `warmup` untimed steps, then `steps` steps between two events
+    (ms per step), with an event pair around every ot_qlinear (mean ms per
+    linear).  Returns (step function, ms per step, per-linear ms, wall s)."""
+    nl = len(layers)
+    ev_q = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+             for _ in range(nl)] for _ in range(steps)]
+
+    def step(events=None):
+        for i, L in enumerate(layers):
+            ot.ot_quantize_act(L["X"], wl.a_bits, L["z"], L["inv_s"], L["Xq"])
+            if events is not None:
+                events[i][0].record()
+            ot.ot_qlinear(L["Xq"], L["Wq"], L["sW"], L["bp"], wl.a_bits, wl.w_bits, L["Y"])
+            if events is not None:
+                events[i][1].record()
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    start.record()
+    for k in range(steps):
+        step(ev_q[k])
+    end.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_step = start.elapsed_time(end) / steps
+    per_layer_ms = [float(np.mean([ev_q[k][i][0].elapsed_time(ev_q[k][i][1])
+                                   for k in range(steps)])) for i in range(nl)]
+    return step, ms_step, per_layer_ms, wall
+
+
+def with_buffers(torch, wl, layers, M):
+    for L in layers:
+        L["a_bits"] = wl.a_bits
+        L["Xq"] = torch.empty((M, L["K"]), dtype=torch.int8, device="cuda")
+        L["Y"] = torch.empty((M, L["N"]), dtype=torch.float16, device="cuda")
+    return layers
+
+
+# The paper's own speed and memory figures (Sec. 4.3, Fig. 3 and Table 5),
+# measured end to end on whole OPT models on the hardware it names (two
+# NVIDIA A100 GPUs, the variant not stated), against FP16: context for the
+# per-linear figures here, not a target.
+PAPER_CONTEXT = {
+    "hardware": "2x NVIDIA A100 (as the paper states it), PyTorch",
+    "end_to_end_speedup_vs_fp16": {"opt6.7b": 1.38, "opt13b": 1.48,
+                                   "workload": "batch 1, 512 tokens (Sec. 4.3, Fig. 3)"},
+    "memory_vs_fp16": "about 2x smaller (Sec. 4.3)",
+    "decode_ms_per_token_fp16_to_ours": {"opt6.7b_bs8": [12.1, 8.2], "opt6.7b_bs16": [11.2, 8.1],
+                                         "opt13b_bs8": [21.9, 15.6], "opt13b_bs16": [19.1, 14.3],
+                                         "workload": "128-token sequences (Table 5)"},
+}
+
+
+def other_prefill_report(torch, ot, synth, name, pool, steps, warmup, iters, with_fp16):
+    """Another prefill workload's four-linear step, timed like the headline
+    one: GEMM TOPS and fraction of the int8 peak per linear and in total,
+    the step with quantization, torch's fp16 linear on the same shapes
+    (speedup) and the weight memory against fp16 (int8 codes + fp32 sW and
+    b' against fp16 W and b)."""
+    wl = synth.WORKLOADS[name]
+    M = wl.M
+    t0 = time.perf_counter()
+    layers = with_buffers(torch, wl, prepare(wl, M, torch, ot, synth, pool), M)
+    log(f"setup {name} {time.perf_counter() - t0:.1f}s")
+    _, ms_step, per_layer_ms, _ = time_prefill_step(torch, ot, wl, layers, steps, warmup)
+    ops = {L["name"]: 2.0 * M * L["N"] * L["K"] for L in layers}
+    gemm_ms = sum(per_layer_ms)
+    gemm_tops = sum(ops.values()) / (gemm_ms * 1e-3) / 1e12
+    rec = {
+        "tokens": M, "a_bits": wl.a_bits, "w_bits": wl.w_bits,
+        "layers": {L["name"]: [L["K"], L["N"]] for L in layers},
+        "plan": {L["name"]: ot.ot_qlinear_plan(M, L["N"], L["K"]) for L in layers},
+        "qlinear_ms_per_launch": {L["name"]: round(t, 4) for L, t in zip(layers, per_layer_ms)},
+        "qlinear_frac_of_int8_peak_per_launch": {
+            L["name"]: round(ops[L["name"]] / (t * 1e-3) / 1e12 / PEAK_INT8_TOPS, 4)
+            for L, t in zip(layers, per_layer_ms)},
+        "qlinear_ms": round(gemm_ms, 4),
+        "qlinear_tops": round(gemm_tops, 1),
+        "qlinear_frac_of_int8_peak": round(gemm_tops / PEAK_INT8_TOPS, 4),
+        "step_ms": round(ms_step, 4),
+        "step_tops": round(sum(ops.values()) / (ms_step * 1e-3) / 1e12, 1),
+        "tokens_per_s": round(M / (ms_step * 1e-3), 1),
+        "weight_bytes": sum(L["K"] * L["N"] + 8 * L["N"] for L in layers),
+        "fp16_weight_bytes": sum(2 * L["K"] * L["N"] + 2 * L["N"] for L in layers),
+    }
+    rec["weight_memory_ratio_vs_fp16"] = round(rec["fp16_weight_bytes"] / rec["weight_bytes"], 4)
+    if with_fp16:
+        fb = fp16_baseline(torch, layers, M, iters)
+        rec["fp16_linear_ms"] = round(fb["ms_per_stack"], 4)
+        rec["fp16_linear_tflops"] = round(fb["tflops"], 1)
+        rec["speedup_of_step_vs_fp16"] = round(fb["ms_per_stack"] / ms_step, 4)
+        rec["speedup_of_qlinear_vs_fp16"] = round(fb["ms_per_stack"] / gemm_ms, 4)
+    log(f"{name}: qlinear {gemm_ms:.3f} ms ({gemm_tops:.0f} TOPS, "
+        f"{100 * gemm_tops / PEAK_INT8_TOPS:.1f} % of peak); step {ms_step:.3f} ms"
+        + (f"; fp16 {rec['fp16_linear_ms']:.3f} ms" if with_fp16 else ""))
+    layers.clear()
+    torch.cuda.empty_cache()
+    return rec
+
+
 def main():
     args = parse()
     if args.traffic_record:
@@ -784,42 +895,13 @@ def main():
     M = wl.M
     pool = cf.ThreadPoolExecutor(max_workers=min(16, os.cpu_count() or 4))
     t_setup = time.perf_counter()
-    layers = prepare(wl, M, torch, ot, synth, pool)
-    for L in layers:
-        L["a_bits"] = wl.a_bits
-        L["Xq"] = torch.empty((M, L["K"]), dtype=torch.int8, device="cuda")
-        L["Y"] = torch.empty((M, L["N"]), dtype=torch.float16, device="cuda")
+    layers = with_buffers(torch, wl, prepare(wl, M, torch, ot, synth, pool), M)
     log(f"setup {time.perf_counter() - t_setup:.1f}s")
 
-    nl = len(layers)
-    ev_q = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-             for _ in range(nl)] for _ in range(args.steps)]
-
-    def step(events=None):
-        for i, L in enumerate(layers):
-            ot.ot_quantize_act(L["X"], wl.a_bits, L["z"], L["inv_s"], L["Xq"])
-            if events is not None:
-                events[i][0].record()
-            ot.ot_qlinear(L["Xq"], L["Wq"], L["sW"], L["bp"], wl.a_bits, wl.w_bits, L["Y"])
-            if events is not None:
-                events[i][1].record()
-
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    t0 = time.perf_counter()
-    start.record()
-    for k in range(args.steps):
-        step(ev_q[k])
-    end.record()
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    ms_step = start.elapsed_time(end) / args.steps
+    step, ms_step, per_layer_ms, wall = time_prefill_step(torch, ot, wl, layers, args.steps,
+                                                          args.warmup)
     ops_step = sum(2.0 * M * L["N"] * L["K"] for L in layers)
     tops = ops_step / (ms_step * 1e-3) / 1e12
-    per_layer_ms = [float(np.mean([ev_q[k][i][0].elapsed_time(ev_q[k][i][1])
-                                   for k in range(args.steps)])) for i in range(nl)]
     gemm_ms = sum(per_layer_ms)
     gemm_tops = ops_step / (gemm_ms * 1e-3) / 1e12
     log(f"step {ms_step:.3f} ms ({tops:.0f} TOPS); qlinear {gemm_ms:.3f} ms ({gemm_tops:.0f} TOPS); "
@@ -884,10 +966,16 @@ def main():
         result["ln_quantize"] = {"workload": wl.name, "bound": "hbm", "peak_GBps": PEAK_HBM_GBS,
                                  "kernel": "ln_quantize_kernel",
                                  "by_layer": ln_quantize_report(torch, ot, synth, wl, args.iters)}
+    layers.clear()
+    torch.cuda.empty_cache()
+    if not args.no_other:
+        result["other_prefill"] = {
+            n: other_prefill_report(torch, ot, synth, n, pool, args.steps, args.warmup,
+                                    args.iters, not args.no_fp16)
+            for n in ("opt6.7b_w8a8", "opt66b_w8a8") if n != wl.name}
+        result["paper_context"] = PAPER_CONTEXT
     if not args.no_decode:
         dwl = synth.WORKLOADS[args.decode_workload]
-        layers.clear()
-        torch.cuda.empty_cache()
         result["decode"] = {"workload": dwl.name, "bound": "hbm", "peak_GBps": PEAK_HBM_GBS,
                             "by_M": decode_report(torch, ot, synth, dwl, pool, args.iters,
                                                   not args.no_fp16)}

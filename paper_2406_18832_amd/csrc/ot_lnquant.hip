@@ -20,9 +20,11 @@
 // chunks, a butterfly across a wave, waves in order), and bounds its own
 // error: a sum whose terms pass through at most n additions is off by at
 // most n 2^-53 times the sum of their magnitudes (and sum |d_k| <=
-// sqrt(K sum d_k^2)).  If the float64 mean and rstd lie farther than that
-// bound (plus the rounding error of the exact procedure itself) from every
-// fp32 rounding boundary, their fp32 roundings are the exact ones.  Rows
+// sqrt(K sum d_k^2)); the few float64 steps after the sums (products with
+// fl(1/K), a Newton-refined reciprocal square root) add a few units each.
+// If the float64 mean and rstd lie farther than that bound (plus the
+// rounding error of the exact procedure itself) from every fp32 rounding
+// boundary, their fp32 roundings are the exact ones.  Rows
 // where they do not (rare: a few in 10^5 on spread-out rows; always for a
 // row whose mean is 0 but whose values are not all 0) take the second way:
 // exact integer sums (S1 in 64 bits, S2 in 128 bits) and the float64 steps
@@ -75,13 +77,39 @@ __device__ inline double u128_to_double(u128 v) {
 
 // True when x and the value it stands for, known to within err, may lie on
 // different sides of a boundary between two fp32 rounding cells, i.e. when
-// fp32(x) is not certain to be the fp32 rounding of that value.
+// fp32(x) is not certain to be the fp32 rounding of that value.  The cell
+// of f = fp32(x) ends halfway to its neighbours, taken from f's bits.
 __device__ inline bool near_fp32_boundary(double x, double err) {
   const float f = (float)x;
-  if (!isfinite(f) || !(err < 1e300)) return true;
-  const double up = 0.5 * ((double)f + (double)nextafterf(f, INFINITY));
-  const double dn = 0.5 * ((double)f + (double)nextafterf(f, -INFINITY));
+  const uint32_t b = __float_as_uint(f);
+  if ((b & 0x7f800000u) == 0x7f800000u || !(err < 1e300)) return true;
+  uint32_t bu, bd;  // the next fp32 values above and below f
+  if ((b & 0x7fffffffu) == 0) {
+    bu = 0x00000001u;
+    bd = 0x80000001u;
+  } else if (b >> 31) {
+    bu = b - 1;
+    bd = b + 1;
+  } else {
+    bu = b + 1;
+    bd = b - 1;
+  }
+  const double up = 0.5 * ((double)f + (double)__uint_as_float(bu));  // exact
+  const double dn = 0.5 * ((double)f + (double)__uint_as_float(bd));
   return x + err >= up || x - err <= dn;
+}
+
+// 1/sqrt(v) to within a few float64 units: the hardware estimate refined
+// by two Newton steps (each at least squares the estimate's relative error
+// and adds about 3 units of rounding).
+__device__ inline double rsqrt_refined(double v) {
+  double r = __builtin_amdgcn_rsq(v);
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const double t = (v * r) * r;
+    r = r * (1.5 - 0.5 * t);
+  }
+  return r;
 }
 
 // Wave-wide exact sums (lane 0 ends with the totals).
@@ -103,8 +131,8 @@ __device__ inline u128 wave_sum_u128(u128 v) {
 template <int CPT, int R, int MAXT>
 __global__ __launch_bounds__(MAXT) void ln_quantize_kernel(
     const uint16_t *__restrict__ h, int64_t M, int K, const uint16_t *__restrict__ gamma,
-    const uint16_t *__restrict__ beta, double eps, float qa, const float *__restrict__ z,
-    const float *__restrict__ inv_s, int8_t *__restrict__ Xq) {
+    const uint16_t *__restrict__ beta, double eps, double inv_k, float qa,
+    const float *__restrict__ z, const float *__restrict__ inv_s, int8_t *__restrict__ Xq) {
   __shared__ double red[2][16][R];  // per wave partial sums of d and d^2
   const int T = blockDim.x;
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6, nwaves = T >> 6;
@@ -169,20 +197,27 @@ __global__ __launch_bounds__(MAXT) void ln_quantize_kernel(
       s1 += red[0][w][r];
       s2 += red[1][w][r];
     }
-    const double dm = s1 / (double)K;  // mean - c
+    // the fast path only has to land within the bound below of the exact
+    // procedure, so it takes the cheap operations: products with a rounded
+    // 1/K and a refined reciprocal square root
+    const double dm = s1 * inv_k;  // mean - c
+    const double q = s2 * inv_k;   // sum d^2 / K
     const double mean = cs[r] + dm;
-    const double var = fmax(s2 / (double)K - dm * dm, 0.0);
+    const double var = fmax(q - dm * dm, 0.0);
     const double ve = var + eps;
-    const double rstd = 1.0 / sqrt(ve);
+    const double rstd = rsqrt_refined(ve);
     mu32[r] = (float)mean;
     r32[r] = (float)rstd;
-    // error bounds against the exact procedure (its own roundings included)
-    const double rms = sqrt(s2 / (double)K) * (1.0 + 1e-9);   // >= sum |d_k| / K
-    const double e_dm = gam * rms + kU * fabs(dm);
+    // error bounds against the exact procedure, its own roundings included;
+    // rms >= sqrt(sum d^2 / K) >= sum |d| / K (sqrt to within one fp32 unit)
+    const double rms = (double)(__builtin_amdgcn_sqrtf((float)q) * 1.0001f);
+    const double e_dm = gam * rms + 2.01 * kU * fabs(dm);
     const double e_mean = 1.1 * (e_dm + 4.0 * kU * fabs(mean));
-    const double e_var = 1.1 * ((gam + 2.0 * kU) * rms * rms + (2.0 * fabs(dm) + 2.0 * e_dm) * e_dm +
+    const double e_var = 1.1 * ((gam + 3.0 * kU) * rms * rms + (2.0 * fabs(dm) + 2.0 * e_dm) * e_dm +
                                 kU * dm * dm + 4.0 * kU * var);
-    const double e_rstd = rstd * (0.55 * (e_var + 3.0 * kU * ve) / ve + 6.0 * kU);
+    // relative change of rstd: half that of var + eps (1 / (var + eps) =
+    // rstd^2), plus the roundings of both square roots and reciprocals
+    const double e_rstd = rstd * (0.55 * (e_var * rstd * rstd + 3.0 * kU) + 20.0 * kU);
     exact[r] = row0 + r < M &&
                (near_fp32_boundary(mean, e_mean) || near_fp32_boundary(rstd, e_rstd));
     any_exact |= exact[r];
@@ -300,8 +335,8 @@ hipError_t launch_lnq(const uint16_t *h, int64_t M, int64_t K, const uint16_t *g
   const int threads = (int)((nchunks + CPT * 64 - 1) / (CPT * 64)) * 64;
   if (threads > MAXT) return hipErrorInvalidValue;
   const unsigned grid = (unsigned)((M + R - 1) / R);
-  ln_quantize_kernel<CPT, R, MAXT><<<grid, threads, 0, st>>>(h, M, (int)K, gamma, beta,
-                                                             (double)eps, (float)qa, z, inv_s, Xq);
+  ln_quantize_kernel<CPT, R, MAXT><<<grid, threads, 0, st>>>(
+      h, M, (int)K, gamma, beta, (double)eps, 1.0 / (double)K, (float)qa, z, inv_s, Xq);
   return hipGetLastError();
 }
 
