@@ -469,9 +469,13 @@ __global__ __launch_bounds__(64 * NR * NK) void qgemm_decode_split_kernel(
                                                    part_rs, per);
 }
 
-// Adds the split runs' partial sums (in run order; integer sums, so any order
-// gives the same result) and applies the epilogue: thread t takes channels
-// 4 (t mod N4) .. +3 of token t / N4.
+// Adds the split runs' partial sums (integer sums, so any order gives the
+// same result) and applies the epilogue: thread t takes channels
+// 4 (t mod N4) .. +3 of token t / N4.  Every run's 16-byte partial is
+// loaded before any is added (at most kMaxRuns runs), so the loads are in
+// flight together.
+constexpr int kMaxRuns = 8;
+
 template <int EPI>
 __global__ __launch_bounds__(256) void decode_reduce_kernel(
     const int32_t *__restrict__ part, const int32_t *__restrict__ part_rs, int splits,
@@ -482,18 +486,27 @@ __global__ __launch_bounds__(256) void decode_reduce_kernel(
   const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (t >= (int64_t)M * n4) return;
   const int m = (int)(t / n4), n = 4 * (int)(t % n4);
+  const int64_t run_stride = (int64_t)M * N;
+  const int32_t *src = part + (int64_t)m * N + n;
   int a[4] = {0, 0, 0, 0};
   int rs = 0;
-  for (int s = 0; s < splits; ++s) {
-    const int32_t *src = part + ((int64_t)s * M + m) * N + n;
-    if (n + 3 < N && (N & 3) == 0) {
-      const v4i v = *reinterpret_cast<const v4i *>(src);
-      a[0] += v[0]; a[1] += v[1]; a[2] += v[2]; a[3] += v[3];
-    } else {
+  if (n + 3 < N && (N & 3) == 0) {
+    v4i v[kMaxRuns];
+#pragma unroll
+    for (int s = 0; s < kMaxRuns; ++s)
+      if (s < splits) v[s] = *reinterpret_cast<const v4i *>(src + s * run_stride);
+#pragma unroll
+    for (int s = 0; s < kMaxRuns; ++s)
+      if (s < splits) {
+        a[0] += v[s][0]; a[1] += v[s][1]; a[2] += v[s][2]; a[3] += v[s][3];
+      }
+  } else {
+    for (int s = 0; s < splits; ++s)
       for (int e = 0; e < 4; ++e)
-        if (n + e < N) a[e] += src[e];
-    }
-    if constexpr (EPI == kEpiAsym) rs += part_rs[(int64_t)s * M + m];
+        if (n + e < N) a[e] += src[s * run_stride + e];
+  }
+  if constexpr (EPI == kEpiAsym) {
+    for (int s = 0; s < splits; ++s) rs += part_rs[(int64_t)s * M + m];
   }
   const float sx = EPI == kEpiToken ? sX[m] : 0.f;
   store4<EPI>(Y, acc_out, sW, bp, zW, sx, rs, m, n, M, N, a[0], a[1], a[2], a[3]);
@@ -630,7 +643,7 @@ static DecodePlan decode_plan(int64_t M, int64_t N, int64_t K, int64_t cus, bool
   for (int rows : {32, 64, 96, 128}) {
     const int64_t tiles = (N + rows - 1) / rows;
     if (tiles > cus) continue;
-    for (int runs = 1; runs <= (split ? 8 : 1) && tiles * runs <= cus; ++runs) {
+    for (int runs = 1; runs <= (split ? kMaxRuns : 1) && tiles * runs <= cus; ++runs) {
       if (runs > 1 && k256 < 4 * runs) break;  // runs of at least 1 KiB of K
       const double t = plan_cost(M, N, K, rows, runs, cus);
       if (best_t == 0 || t < best_t) {
