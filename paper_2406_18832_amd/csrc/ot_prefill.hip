@@ -440,17 +440,20 @@ using namespace detail;
 // proportional to its products over K plus its epilogue, which costs about
 // as much as 820 more K steps, times a factor per tile shape for the operand
 // bytes it stages per product: 0.97 for the wider tile (fewer bytes per
-// product), 1.5 for the shorter one (1.5 times the bytes).  Measured on
-// MI355X, per pass against 256 x 256 at the OPT-6.7B, -13B and -66B layer
-// shapes: 0.93-1.01 and 1.3-1.6.
+// product), 1.5 for the shorter one (1.5 times the bytes), 1.15 for the
+// narrower one (1.17 times).  Measured on MI355X, per pass against 256 x 256
+// at the OPT-6.7B, -13B and -66B layer shapes: 0.93-1.01, 1.3-1.6 and, for
+// 192 x 256, the cheapest tile wherever the model picks it (2048 tokens by
+// 12288 channels: 103.7 against 116.1 us; one-pass launches of 2000 tokens
+// by 5000 channels: equal to 256 x 256 within 4 %).
 static double prefill_cost(int64_t M, int64_t N, int64_t K, int bn, int bm, int cus) {
   const int64_t tiles = ((M + bm - 1) / bm) * ((N + bn - 1) / bn);
   const int64_t passes = (tiles + cus - 1) / cus;
-  const double penalty = bn == 320 ? 0.97 : bm == 128 ? 1.5 : 1.0;
+  const double penalty = bn == 320 ? 0.97 : bn == 192 ? 1.15 : bm == 128 ? 1.5 : 1.0;
   return (double)passes * bn * bm * ((double)K + 820.0) * penalty;
 }
 
-// Three tile shapes, each one workgroup of 8 waves per CU with a 2-stage
+// Four tile shapes, each one workgroup of 8 waves per CU with a 2-stage
 // ring of BK = 128:
 //   256 (channels) x 256 (tokens), waves 4 x 2 of 64 x 128 (128 KiB of LDS);
 //   320 x 256, waves 2 x 4 of 160 x 64 (144 KiB): lets layers whose tile
@@ -459,16 +462,21 @@ static double prefill_cost(int64_t M, int64_t N, int64_t K, int bn, int bm, int 
 //     and 960 of 256 x 256);
 //   256 x 128, waves 4 x 2 of 64 x 64 (96 KiB): for launches that fill less
 //     than one pass with 256 x 256 (2048 tokens by 4096 channels: 256 tiles
-//     against 128).
+//     against 128);
+//   192 x 256, waves 2 x 4 of 96 x 64 (112 KiB): the same for launches
+//     whose last pass of 256 x 256 runs half empty (2048 tokens by 12288
+//     channels: two full passes of 512 tiles against 1.5 of 384).
 // The cheapest by prefill_cost runs; all give identical results.
-enum class PrefillTile { k256x256, k320x256, k256x128 };
+enum class PrefillTile { k256x256, k320x256, k256x128, k192x256 };
 
 static PrefillTile prefill_tile(int64_t M, int64_t N, int64_t K) {
   const int cus = device_cus();
   const double c0 = prefill_cost(M, N, K, 256, 256, cus);
   const double c1 = prefill_cost(M, N, K, 320, 256, cus);
   const double c2 = prefill_cost(M, N, K, 256, 128, cus);
-  if (c1 < c0 && c1 <= c2) return PrefillTile::k320x256;
+  const double c3 = prefill_cost(M, N, K, 192, 256, cus);
+  if (c1 < c0 && c1 <= c2 && c1 <= c3) return PrefillTile::k320x256;
+  if (c3 < c0 && c3 <= c2) return PrefillTile::k192x256;
   if (c2 < c0) return PrefillTile::k256x128;
   return PrefillTile::k256x256;
 }
@@ -477,6 +485,7 @@ const char *prefill_tile_name(int64_t M, int64_t N, int64_t K) {
   switch (prefill_tile(M, N, K)) {
     case PrefillTile::k320x256: return "prefill 320x256";
     case PrefillTile::k256x128: return "prefill 256x128";
+    case PrefillTile::k192x256: return "prefill 192x256";
     default: return "prefill 256x256";
   }
 }
@@ -491,6 +500,9 @@ hipError_t launch_qgemm_prefill(const int8_t *Xq, const int8_t *Wq, const float 
                                                     acc_out, st);
     case PrefillTile::k256x128:
       return launch_prefill<256, 128, 128, 4, 2, 2>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y,
+                                                    acc_out, st);
+    case PrefillTile::k192x256:
+      return launch_prefill<192, 256, 128, 2, 4, 2>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y,
                                                     acc_out, st);
     default:
       return launch_prefill<256, 256, 128, 4, 2, 2>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y,

@@ -270,16 +270,18 @@ def test_pipeline_opt125m(a_bits, w_bits):
 
 # --------------------------------------------------------------------------
 # Prefill tile shapes and the LDS-staged epilogue (Y only, no acc_out): the
-# library runs 256 x 256, 320 (channels) x 256 (tokens) or 256 x 128 tiles,
-# whichever fills the compute units best.  On a 256-CU MI355X the shapes
-# below take, in order, the 320 x 256 tile (256 tiles against 320 of
-# 256 x 256), the 256 x 128 tile (less than one pass either way) and the
-# 256 x 256 tile (160 tiles, against two passes of 256 x 128); all have
-# ragged M, N and K.
+# library runs 256 x 256, 320 (channels) x 256 (tokens), 256 x 128 or
+# 192 x 256 tiles, whichever its cost model prices lowest.  On a 256-CU
+# MI355X the shapes below take, in order, the 320 x 256 tile (256 tiles
+# against 320 of 256 x 256), the 256 x 128 tile (less than one pass either
+# way), the 192 x 256 tile (one pass, 216 tiles) and the 256 x 256 tile
+# (two passes: 205 x 2, against three of 192 x 256); all have ragged M, N
+# and K.
 # --------------------------------------------------------------------------
-PREFILL_TILE_SHAPES = [(500, 40860, 272), (300, 1000, 1040), (2000, 5000, 272)]
+PREFILL_TILE_SHAPES = [(500, 40860, 272), (300, 1000, 1040), (2000, 5000, 272), (1025, 9831, 272)]
 PREFILL_TILE_ON_256_CUS = {(500, 40860, 272): "prefill 320x256", (300, 1000, 1040): "prefill 256x128",
-                           (2000, 5000, 272): "prefill 256x256"}
+                           (2000, 5000, 272): "prefill 192x256",
+                           (1025, 9831, 272): "prefill 256x256"}
 
 
 def test_prefill_tiles_all_covered():
