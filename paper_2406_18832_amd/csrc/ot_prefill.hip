@@ -25,7 +25,12 @@ namespace detail {
 // cores work on one 32-byte K step the fragments of the next are in flight.
 // The one barrier per K tile sits between the last fragment reads of tile t
 // and its last MFMAs; right after it the wave starts reading tile t+1 and
-// refills tile t's stage with tile t+S.
+// refills tile t's stage with tile t+S.  The refill's loads are not issued
+// in one burst: one follows every MPL-th MFMA, over the tile's last K step
+// and the next tile's first ones.  Issued back to back after the barrier,
+// the loads of both waves of a SIMD held its matrix core idle (a load
+// instruction takes the wave's issue for tens of cycles); spread between
+// the MFMAs their issue overlaps the matrix work.
 template <int BN, int BM, int BK, int WN, int WM, int S>
 struct PrefillCfg {
   static constexpr int kWaves = WN * WM;
@@ -59,27 +64,9 @@ __device__ __forceinline__ int swz(int r) {
   else return (r & 7) ^ ((r >> 3) & 1);
 }
 
-// Scheduling recipe for one K step: DS reads (the next step's fragments) and
-// buffer loads spread one by one between the MFMAs, then the rest of the
-// MFMAs, so the matrix cores never wait on the LDS latency.
-template <int kReads, int kMfma, int kVmem>
-__device__ __forceinline__ void sched_interleave() {
-  constexpr int kMask_MFMA = 0x008, kMask_VMEM_READ = 0x020, kMask_DS_READ = 0x100;
-  constexpr int kPaired = kReads < kMfma ? kReads : kMfma;
-#pragma unroll
-  for (int i = 0; i < kPaired; ++i) {
-    if (i < kVmem) __builtin_amdgcn_sched_group_barrier(kMask_VMEM_READ, 1, 0);
-    __builtin_amdgcn_sched_group_barrier(kMask_DS_READ, 1, 0);
-    __builtin_amdgcn_sched_group_barrier(kMask_MFMA, 1, 0);
-  }
-#pragma unroll
-  for (int i = kPaired; i < kVmem; ++i) __builtin_amdgcn_sched_group_barrier(kMask_VMEM_READ, 1, 0);
-  if (kMfma > kPaired) __builtin_amdgcn_sched_group_barrier(kMask_MFMA, kMfma - kPaired, 0);
-}
-
 // The kernel body lives in a device function: hipcc drops the host stub of a
 // kernel template whose body holds lambdas.
-template <int BN, int BM, int BK, int WN, int WM, int S, int EPI>
+template <int BN, int BM, int BK, int WN, int WM, int S, int EPI, int MPL>
 __device__ __forceinline__ void prefill_body(
     int8_t *smem, const int8_t *__restrict__ Xq, const int8_t *__restrict__ Wq,
     const float *__restrict__ sX, const int32_t *__restrict__ zW, const float *__restrict__ sW,
@@ -196,21 +183,73 @@ __device__ __forceinline__ void prefill_body(
   int rs[C::kFM];
 #pragma unroll
   for (int g = 0; g < C::kFM; ++g) rs[g] = 0;
-  auto mfmas = [&](int buf, int step) {
+  // ---- main loop ----------------------------------------------------------------
+  // One 1 KiB load of tile kt's stage: j < kLoadsA a weight load, else a
+  // token load (the j-th of issue_tile's order).
+  auto issue_one = [&](int kt, int j) {
+    int kr = kt;
+    if (kt < KT) {
+      kr = kt + phi;
+      if (kr >= KT) kr -= KT;
+    }
+    const int k0 = kr * BK;
+    int8_t *sa = smem + (kt % S) * C::kStage;
+    if (j < C::kLoadsA) {
+      const int ja = j < C::kLoadsA ? j : 0;  // j is a constant once unrolled
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          rsrc_a, (lds_void *)(sa + (wave * C::kLoadsA + ja) * 1024), 16,
+          k0 + ck_a[ja] * 16 < K ? off_a[ja] + (uint32_t)k0 : kOobOffset, 0, 0, 0);
+    } else {
+      const int jb = j >= C::kLoadsA && j < C::kLoads ? j - C::kLoadsA : 0;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          rsrc_b, (lds_void *)(sa + C::kABytes + (wave * C::kLoadsB + jb) * 1024), 16,
+          k0 + ck_b[jb] * 16 < K ? off_b[jb] + (uint32_t)k0 : kOobOffset, 0, 0, 0);
+    }
+  };
+  // A tile's last K step issues the first kLast loads of the tile S ahead
+  // (whose stage the barrier before it has just freed), one after every
+  // MPL-th MFMA; the next tile's first K steps issue the rest at the same
+  // rate, all before the wait that precedes its last step.
+  constexpr int kMfma = C::kFN * C::kFM;
+  constexpr int kReads = C::kFN + C::kFM;
+  constexpr int kPerStep = kMfma / MPL;
+  constexpr int kLast = kPerStep < C::kLoads ? kPerStep : C::kLoads;
+  static_assert(kPerStep >= 1, "at least one load per K step");
+  static_assert(kLast + (C::kKSteps - 2) * kPerStep >= C::kLoads,
+                "every load of a tile is issued before the wait for it");
+  // One K step: the MFMAs of K step `step` on fragment buffer cb, the
+  // fragment reads of tile rkt's K step rstep into buffer nb, and loads
+  // j0 .. j0+nl-1 of tile lt, issued in that interleaved order (a read
+  // before each MFMA while reads remain, a load after every MPL-th).
+  auto kstep = [&](int cb, int step, int rkt, int rstep, int nb, int lt, int j0, int nl) {
+    const int8_t *st = smem + (rkt % S) * C::kStage;
 #pragma unroll
-    for (int f = 0; f < C::kFN; ++f)
-#pragma unroll
-      for (int g = 0; g < C::kFM; ++g)
-        acc[f][g] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fa[buf][f], fb[buf][g], acc[f][g], 0, 0, 0);
+    for (int i = 0; i < kMfma; ++i) {
+      if (i < C::kFN)
+        fa[nb][i] = *reinterpret_cast<const v4i *>(st + a_base + i * 32 * BK + frag_off[rstep]);
+      else if (i < kReads)
+        fb[nb][i - C::kFN] =
+            *reinterpret_cast<const v4i *>(st + b_base + (i - C::kFN) * 32 * BK + frag_off[rstep]);
+      const int f = i / C::kFM, g = i % C::kFM;
+      acc[f][g] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fa[cb][f], fb[cb][g], acc[f][g], 0, 0, 0);
+      if (i % MPL == MPL - 1 && i / MPL < nl) issue_one(lt, j0 + i / MPL);
+    }
     if constexpr (EPI == kEpiAsym) {
       if (step % WN == __builtin_amdgcn_readfirstlane(wn)) {
 #pragma unroll
-        for (int g = 0; g < C::kFM; ++g) rs[g] = byte_sum16(fb[buf][g], rs[g]);
+        for (int g = 0; g < C::kFM; ++g) rs[g] = byte_sum16(fb[cb][g], rs[g]);
       }
+    }
+    // keep that order through the scheduler
+    constexpr int kMaskMfma = 0x008, kMaskVmemRead = 0x020, kMaskDsRead = 0x100;
+#pragma unroll
+    for (int i = 0; i < kMfma; ++i) {
+      if (i < kReads) __builtin_amdgcn_sched_group_barrier(kMaskDsRead, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(kMaskMfma, 1, 0);
+      if (i % MPL == MPL - 1 && i / MPL < nl) __builtin_amdgcn_sched_group_barrier(kMaskVmemRead, 1, 0);
     }
   };
 
-  // ---- main loop ----------------------------------------------------------------
   // Tiles past the end of K are issued too, as out-of-range loads that land
   // zeros in a stage nobody reads: every iteration then has the same number
   // of loads in flight and one fixed wait, with no branches in the loop.
@@ -218,31 +257,29 @@ __device__ __forceinline__ void prefill_body(
   for (int t = 0; t < S - 1; ++t) issue_tile(t);
   wait_vmcnt<(S - 2) * C::kLoads>();  // tile 0 has landed
   lds_barrier();
-  issue_tile(S - 1);
+#pragma unroll
+  for (int j = 0; j < kLast; ++j) issue_one(S - 1, j);
   read_frags(0, 0, 0);
 
   for (int kt = 0; kt < KT; ++kt) {
 #pragma unroll
     for (int s = 0; s + 1 < C::kKSteps; ++s) {
-      read_frags(kt, s + 1, (s + 1) & 1);
-      mfmas(s & 1, s);
-      // keep the next step's fragment reads spread over this step's MFMAs
-      sched_interleave<C::kFN + C::kFM, C::kFN * C::kFM, 0>();
+      const int j0 = kLast + s * kPerStep;
+      const int nl = j0 >= C::kLoads ? 0 : (C::kLoads - j0 < kPerStep ? C::kLoads - j0 : kPerStep);
+      kstep(s & 1, s, kt, s + 1, (s + 1) & 1, kt + S - 1, j0, nl);
     }
     // This wave's reads of tile kt are complete once lgkmcnt drains; tile
     // kt+1 has landed once at most S-2 younger tiles (kt+2 .. kt+S-1) are in
     // flight.  After the barrier every wave is past tile kt, so its stage
     // takes tile kt+S.  At kt = KT-1 the reads of "tile KT" are unused.
-    // The scheduling fence keeps every MFMA of the steps above ahead of the
+    // The scheduling fences keep every MFMA of the steps above ahead of the
     // wait, so the reads have that long to land.
     __builtin_amdgcn_sched_barrier(0);
     __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
     wait_vmcnt<(S - 2) * C::kLoads>();
     lds_barrier();
-    issue_tile(kt + S);
-    read_frags(kt + 1, 0, 0);
-    mfmas(1, C::kKSteps - 1);
-    sched_interleave<C::kFN + C::kFM, C::kFN * C::kFM, C::kLoads>();
+    kstep(1, C::kKSteps - 1, kt + 1, 0, 0, kt + S, 0, kLast);
+    __builtin_amdgcn_sched_barrier(0);
   }
   wait_vmcnt<0>();
 
@@ -398,7 +435,7 @@ __device__ __forceinline__ void prefill_body(
 
 }
 
-template <int BN, int BM, int BK, int WN, int WM, int S, int OCC, int EPI>
+template <int BN, int BM, int BK, int WN, int WM, int S, int MPL, int OCC, int EPI>
 __global__ __launch_bounds__(64 * WN * WM, OCC) void qgemm_prefill_kernel(
     const int8_t *__restrict__ Xq, const int8_t *__restrict__ Wq, const float *__restrict__ sX,
     const int32_t *__restrict__ zW, const float *__restrict__ sW, const float *__restrict__ bp,
@@ -406,13 +443,13 @@ __global__ __launch_bounds__(64 * WN * WM, OCC) void qgemm_prefill_kernel(
     int tiles_n, int group_m) {
   __shared__ __attribute__((aligned(1024)))
   int8_t smem[S * PrefillCfg<BN, BM, BK, WN, WM, S>::kStage];
-  prefill_body<BN, BM, BK, WN, WM, S, EPI>(smem, Xq, Wq, sX, zW, sW, bp, M, N, K, Y, acc_out,
+  prefill_body<BN, BM, BK, WN, WM, S, EPI, MPL>(smem, Xq, Wq, sX, zW, sW, bp, M, N, K, Y, acc_out,
                                            tiles_m, tiles_n, group_m);
 }
 
 // Epilogue by argument: sX != nullptr per-token scales sX [M]; zW != nullptr
 // asymmetric weight zero points zW [N]; neither: per-channel.
-template <int BN, int BM, int BK, int WN, int WM, int S, int OCC = 1>
+template <int BN, int BM, int BK, int WN, int WM, int S, int MPL, int OCC = 1>
 hipError_t launch_prefill(const int8_t *Xq, const int8_t *Wq, const float *sX, const int32_t *zW,
                           const float *sW, const float *bp, int64_t M, int64_t N, int64_t K,
                           uint16_t *Y, int32_t *acc_out, hipStream_t st, int group_m = 8) {
@@ -420,13 +457,13 @@ hipError_t launch_prefill(const int8_t *Xq, const int8_t *Wq, const float *sX, c
   const unsigned grid = (unsigned)(tiles_m * tiles_n);
   const dim3 block(64 * WN * WM);
   if (sX)
-    qgemm_prefill_kernel<BN, BM, BK, WN, WM, S, OCC, kEpiToken><<<grid, block, 0, st>>>(
+    qgemm_prefill_kernel<BN, BM, BK, WN, WM, S, MPL, OCC, kEpiToken><<<grid, block, 0, st>>>(
         Xq, Wq, sX, zW, sW, bp, (int)M, (int)N, (int)K, Y, acc_out, tiles_m, tiles_n, group_m);
   else if (zW)
-    qgemm_prefill_kernel<BN, BM, BK, WN, WM, S, OCC, kEpiAsym><<<grid, block, 0, st>>>(
+    qgemm_prefill_kernel<BN, BM, BK, WN, WM, S, MPL, OCC, kEpiAsym><<<grid, block, 0, st>>>(
         Xq, Wq, sX, zW, sW, bp, (int)M, (int)N, (int)K, Y, acc_out, tiles_m, tiles_n, group_m);
   else
-    qgemm_prefill_kernel<BN, BM, BK, WN, WM, S, OCC, kEpiChannel><<<grid, block, 0, st>>>(
+    qgemm_prefill_kernel<BN, BM, BK, WN, WM, S, MPL, OCC, kEpiChannel><<<grid, block, 0, st>>>(
         Xq, Wq, sX, zW, sW, bp, (int)M, (int)N, (int)K, Y, acc_out, tiles_m, tiles_n, group_m);
   return hipGetLastError();
 }
@@ -445,7 +482,9 @@ using namespace detail;
 // at the OPT-6.7B, -13B and -66B layer shapes: 0.93-1.01, 1.3-1.6 and, for
 // 192 x 256, the cheapest tile wherever the model picks it (2048 tokens by
 // 12288 channels: 103.7 against 116.1 us; one-pass launches of 2000 tokens
-// by 5000 channels: equal to 256 x 256 within 4 %).
+// by 5000 channels: equal to 256 x 256 within 4 %).  Re-measured with the
+// loads spread over the MFMAs (OPT-6.7B and -13B shapes): 1.01, 1.61 and
+// 1.24, which pick the same tiles on those layers.
 static double prefill_cost(int64_t M, int64_t N, int64_t K, int bn, int bm, int cus) {
   const int64_t tiles = ((M + bm - 1) / bm) * ((N + bn - 1) / bn);
   const int64_t passes = (tiles + cus - 1) / cus;
@@ -496,16 +535,16 @@ hipError_t launch_qgemm_prefill(const int8_t *Xq, const int8_t *Wq, const float 
                                 hipStream_t st) {
   switch (prefill_tile(M, N, K)) {
     case PrefillTile::k320x256:
-      return launch_prefill<320, 256, 128, 2, 4, 2>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y,
+      return launch_prefill<320, 256, 128, 2, 4, 2, 2>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y,
                                                     acc_out, st);
     case PrefillTile::k256x128:
-      return launch_prefill<256, 128, 128, 4, 2, 2>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y,
+      return launch_prefill<256, 128, 128, 4, 2, 2, 1>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y,
                                                     acc_out, st);
     case PrefillTile::k192x256:
-      return launch_prefill<192, 256, 128, 2, 4, 2>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y,
+      return launch_prefill<192, 256, 128, 2, 4, 2, 2>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y,
                                                     acc_out, st);
     default:
-      return launch_prefill<256, 256, 128, 4, 2, 2>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y,
+      return launch_prefill<256, 256, 128, 4, 2, 2, 2>(Xq, Wq, sX, zW, sW, bprime, M, N, K, Y,
                                                     acc_out, st);
   }
 }
