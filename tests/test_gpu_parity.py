@@ -276,12 +276,18 @@ def test_pipeline_opt125m(a_bits, w_bits):
 # against 320 of 256 x 256), the 256 x 128 tile (less than one pass either
 # way), the 192 x 256 tile (one pass, 216 tiles) and the 256 x 256 tile
 # (two passes: 205 x 2, against three of 192 x 256); all have ragged M, N
-# and K.
+# and K.  The last two repeat the 320 x 256 and 256 x 256 cases with whole
+# 16-byte output rows (N a multiple of 8), where the tiles inside M x N take
+# the epilogue without per-lane bounds checks and the edge tiles the checked
+# one.
 # --------------------------------------------------------------------------
-PREFILL_TILE_SHAPES = [(500, 40860, 272), (300, 1000, 1040), (2000, 5000, 272), (1025, 9831, 272)]
+PREFILL_TILE_SHAPES = [(500, 40860, 272), (300, 1000, 1040), (2000, 5000, 272), (1025, 9831, 272),
+                       (500, 40864, 272), (1025, 9832, 272)]
 PREFILL_TILE_ON_256_CUS = {(500, 40860, 272): "prefill 320x256", (300, 1000, 1040): "prefill 256x128",
                            (2000, 5000, 272): "prefill 192x256",
-                           (1025, 9831, 272): "prefill 256x256"}
+                           (1025, 9831, 272): "prefill 256x256",
+                           (500, 40864, 272): "prefill 320x256",
+                           (1025, 9832, 272): "prefill 256x256"}
 
 
 def test_prefill_tiles_all_covered():
