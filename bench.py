@@ -482,9 +482,10 @@ def traffic_record(d, workload):
             raise SystemExit(f"{len(disp)} prefill dispatches is not a whole number of steps")
         for i, (g, v) in enumerate(disp):
             L = wl.layers[i % len(wl.layers)]
-            # the library runs 256 x 256, 320 (channels) x 256 (tokens) or 256 x 128 tiles
+            # the library runs 256 x 256, 320 (channels) x 256 (tokens), 256 x 128 or
+            # 192 x 256 tiles
             grids = {f"{bn}x{bm}": -(-wl.M // bm) * -(-L.N // bn) * threads
-                     for bn, bm in ((256, 256), (320, 256), (256, 128))}
+                     for bn, bm in ((256, 256), (320, 256), (256, 128), (192, 256))}
             match = [t for t, gg in grids.items() if gg == g]
             if not match:
                 raise SystemExit(f"dispatch {i}: grid {g} fits no tile shape of layer {L.name} "
@@ -502,9 +503,9 @@ def traffic_record(d, workload):
         alg[L.name] = wl.M * L.K + L.N * L.K + 2 * wl.M * L.N + 8 * L.N
     cmd = "cd /tmp && timeout -s KILL 120 rocprofv3 --pmc {c} --output-format csv -d <out>/{sub} -o p -- python -u <repo>/bench.py {args}"
     bench_args = ("--steps 2 --warmup 1 --no-cpu --no-fp16 --no-decode --no-ln --no-mixed "
-                  "--no-asym --no-sclk")
+                  "--no-asym --no-sclk --no-other")
     rec = {
-        "kernel": "qgemm_prefill_kernel (256x256, 320x256 or 256x128 tiles, BK 128, 2 stages)",
+        "kernel": "qgemm_prefill_kernel (256x256, 320x256, 256x128 or 192x256 tiles, BK 128, 2 stages)",
         "workload": f"{wl.name} ({wl.M} tokens; " + ", ".join(L.name for L in wl.layers) + ")",
         "source_files": [os.path.relpath(p, ROOT) for p in PREFILL_SOURCES],
         "source_sha256": prefill_source_digest(),
@@ -576,27 +577,30 @@ def counter_summary(d, workload, decode_workload):
         by = {}
         for r in rows:
             e = by.setdefault(int(r["Dispatch_Id"]), {"name": r["Kernel_Name"],
-                                                      "grid": int(r["Grid_Size"])})
+                                                      "grid": int(r["Grid_Size"]),
+                                                      "ns": int(r["End_Timestamp"])
+                                                      - int(r["Start_Timestamp"])})
             e[r["Counter_Name"]] = e.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
         return [by[k] for k in sorted(by)]
 
     simds, xcds = 1024, 8
     wl = synth.WORKLOADS[workload]
     pre = [e for e in dispatches("mfma") if "qgemm_prefill_kernel" in e["name"]]
-    out = ["| Layer | Tile | int8 ops counted (MOPS_I8 x 512) | 2MNK | MFMA busy / (GUI active x 1024 SIMDs) | LDS bank-conflict cycles / LDS instr |",
-           "|---|---|---|---|---|---|"]
+    out = ["| Layer | Tile | int8 ops counted (MOPS_I8 x 512) | 2MNK | MFMA busy / (GUI active x 1024 SIMDs) | LDS bank-conflict cycles / LDS instr | shader clock: GUI active per XCD / dispatch time |",
+           "|---|---|---|---|---|---|---|"]
     for i, L in enumerate(wl.layers):
         es = pre[i::len(wl.layers)]
         ops = np.mean([e["SQ_INSTS_VALU_MFMA_MOPS_I8"] * 512 for e in es])
         util = np.mean([e["SQ_VALU_MFMA_BUSY_CYCLES"] / (e["GRBM_GUI_ACTIVE"] / xcds * simds)
                         for e in es])
         confl = np.mean([e["SQ_LDS_BANK_CONFLICT"] / max(e["SQ_INSTS_LDS"], 1) for e in es])
+        ghz = np.mean([e["GRBM_GUI_ACTIVE"] / xcds / e["ns"] for e in es])
         tile = "?"
-        for bn, bm in ((256, 256), (320, 256), (256, 128)):
+        for bn, bm in ((256, 256), (320, 256), (256, 128), (192, 256)):
             if es[0]["grid"] == -(-wl.M // bm) * -(-L.N // bn) * 512:
                 tile = f"{bn}x{bm}"
         out.append(f"| {L.name} | {tile} | {ops:.4g} | {2 * wl.M * L.N * L.K:.4g} | {util:.3f} | "
-                   f"{confl:.3f} |")
+                   f"{confl:.3f} | {ghz:.2f} GHz |")
     copy = [e for e in dispatches("dram_copy") if "copyBuffer" in e["name"]]
     n_copy = 1 << 30
     big = [e for e in copy if e["TCC_EA0_RDREQ_DRAM_32B"] * 32 > n_copy / 4]
@@ -634,6 +638,25 @@ def counter_summary(d, workload, decode_workload):
             alg = wl.M * L.K + L.N * L.K + 8 * L.N
             out3.append(f"| {L.name} | {rd / 1e6:.1f} MB | {wr / 1e6:.1f} MB | {alg / 1e6:.1f} MB | "
                         f"{rd / alg:.3f} |")
+    out4 = []
+    if os.path.isdir(os.path.join(d, "diag")):
+        # what the K loop waits on: L1-to-L2 read latency, L2 hit rate and
+        # the vector memory pipeline's busy and stall cycles, per CU per
+        # active cycle
+        pre_g = [e for e in dispatches("diag") if "qgemm_prefill_kernel" in e["name"]]
+        cus = 256
+        out4 = ["| Layer | L1-to-L2 read latency (cycles per request) | L2 hit rate | TA busy | TA address stalled by TC | TCP stalled on pending L2 data |",
+                "|---|---|---|---|---|---|"]
+        for li, L in enumerate(wl.layers):
+            es = pre_g[li::len(wl.layers)]
+
+            def per_cu(key):
+                return np.mean([e[key] / (e["GRBM_GUI_ACTIVE"] / xcds) / cus for e in es])
+            lat = np.mean([e["TCP_TCC_READ_REQ_LATENCY"] / e["TCP_TCC_READ_REQ"] for e in es])
+            hit = np.mean([e["TCC_HIT"] / (e["TCC_HIT"] + e["TCC_MISS"]) for e in es])
+            out4.append(f"| {L.name} | {lat:.0f} | {hit:.3f} | {per_cu('TA_TA_BUSY'):.2f} | "
+                        f"{per_cu('TA_ADDR_STALLED_BY_TC_CYCLES'):.2f} | "
+                        f"{per_cu('TCP_PENDING_STALL_CYCLES'):.2f} |")
     print("\n".join(out))
     print()
     print(f"DRAM counter calibration on a 1 GiB copy: read factor {rd_f:.3f}, write factor {wr_f:.3f}")
@@ -644,6 +667,11 @@ def counter_summary(d, workload, decode_workload):
         print("Prefill step (OPT-13B W6A6), DRAM bytes per launch:")
         print()
         print("\n".join(out3))
+    if out4:
+        print()
+        print("Prefill step (OPT-13B W6A6), what the K loop waits on (mean over the run's launches):")
+        print()
+        print("\n".join(out4))
 
 
 def copy_probe(torch):
@@ -935,16 +963,18 @@ def main():
     if not args.no_sclk:
         clk = shader_clock_window(torch, step)
         if "median_MHz" in clk:
-            # the matrix cores' peak scales with the clock (5.0 POP/s at 2400 MHz)
-            peak_at_clk = PEAK_INT8_TOPS * clk["median_MHz"] / 2400.0
             clk["frac_of_2400_MHz"] = round(clk["median_MHz"] / 2400.0, 4)
-            clk["qlinear_frac_of_mfma_peak_at_this_clock"] = round(gemm_tops / peak_at_clk, 4)
-            log(f"shader clock over {clk['steps']} steps: median {clk['median_MHz']:.0f} MHz; "
-                f"qlinear at {100 * clk['qlinear_frac_of_mfma_peak_at_this_clock']:.0f} % of the "
-                f"MFMA peak at that clock")
+            # What the SMU reports is not the clock the GEMM's waves run at:
+            # counted inside the kernels (shader cycles over the 100 MHz
+            # real-time counter, and GRBM_GUI_ACTIVE over each dispatch's
+            # duration) the prefill GEMMs run at 1.7-2.1 GHz.
+            clk["note"] = ("SMU-reported clock; the GEMM dispatches' own cycle counts give "
+                           "1.7-2.1 GHz (counter summary under profiles/)")
+            log(f"SMU-reported shader clock over {clk['steps']} steps: median "
+                f"{clk['median_MHz']:.0f} MHz")
         else:
             log(f"shader clock: {clk['error']}")
-        result["prefill_shader_clock"] = clk
+        result["prefill_smu_clock"] = clk
     if not args.no_fp16:
         fb = fp16_baseline(torch, layers, M, args.iters)
         fb["speedup_of_step"] = fb["ms_per_stack"] / ms_step
