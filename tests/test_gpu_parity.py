@@ -322,6 +322,27 @@ def test_prefill_tiles_staged_epilogue(M, N, K, flavour):
     assert_fp16_close(host(Y), ref)
 
 
+# Every prefill tile at one and two K tiles (K = 48, 128, 144): the next
+# tiles' operand loads, spread over the MFMAs of the last K step and the
+# following tile's first ones, then all fall past the end of K (zeros into
+# a stage nobody reads), and the checkerboard's odd tiles wrap round at once.
+PREFILL_SHORT_K = [(500, 40864), (2000, 5000), (1025, 9832), (300, 1000)]
+
+
+@pytest.mark.parametrize("M,N", PREFILL_SHORT_K)
+@pytest.mark.parametrize("K", [48, 128, 144])
+def test_prefill_tiles_short_k(M, N, K):
+    Xq, Wq, sW, bp = _random_qlinear_inputs(M, N, K, 8, 8, 5 * M + N + K)
+    case(f"prefill short K M={M} N={N} K={K} plan={ot.ot_qlinear_plan(M, N, K)}")
+    Y, acc = ot.qlinear(dev(Xq), dev(Wq), dev(sW), dev(bp), 8, 8, want_acc=True)
+    ref_acc = O.int_gemm(Xq, Wq)
+    assert np.array_equal(host(acc), ref_acc)
+    Y2 = ot.qlinear(dev(Xq), dev(Wq), dev(sW), dev(bp), 8, 8)  # the staged epilogue
+    ref = O.epilogue(ref_acc, sW, bp)
+    assert_fp16_close(host(Y), ref)
+    assert_fp16_close(host(Y2), ref)
+
+
 # --------------------------------------------------------------------------
 # Split-K decode: 17-64 tokens with at most 32 output channels per CU, given a
 # workspace, split K over more workgroups and add their int32 partial sums in
