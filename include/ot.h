@@ -331,8 +331,9 @@ size_t ot_qlinear_workspace_size(int64_t M, int64_t N, int64_t K);
  * packed != 0, ot_qlinear_packed) launch for these sizes on the current
  * device, given a workspace (with_workspace != 0) or not.  Writes a
  * NUL-terminated description into buf (at most len bytes, truncated if
- * longer): "none" for M == 0; "prefill 256x256", "prefill 320x256" or
- * "prefill 256x128" (output channels x tokens per workgroup) above 64
+ * longer): "none" for M == 0; "prefill 256x256", "prefill 320x256",
+ * "prefill 256x128" or "prefill 192x256" (output channels x tokens per
+ * workgroup) above 64
  * tokens; "decode <layout> <R>-row tiles", with " split-K <runs>" where K
  * is split, up to 64 tokens.  OT_EINVAL for a NULL buf or len 0, OT_ESHAPE
  * for sizes the calls reject.  Synchronous, no device work; for
