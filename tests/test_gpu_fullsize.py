@@ -136,3 +136,84 @@ def test_decode_layer_full(name, li):
         assert_fp16_close(Y.cpu().numpy(), rY[:M], f"Y M={M}")
         assert_fp16_close(Y2.cpu().numpy(), rY[:M], f"Y(acc path) M={M}")
         assert torch.equal(Y3, Y) and torch.equal(Y4, Y), f"Y (workspace, packed) M={M}"
+
+
+# The two other epilogue flavours at full size, on the OPT-13B W6A6 layers
+# (4096 tokens, every element): asymmetric ("Int8") weights, Eq. (a), on
+# all four linears, and the paper's per-token path, Eq. (c), on the two it
+# applies to (out and fc2), as the benchmark's asym_weights and mixed_block
+# steps run them.
+OPT13B = [("opt13b_w6a6", i) for i in range(4)]
+
+
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("name,li", OPT13B)
+def test_prefill_asym_layer_every_element(name, li):
+    wl = synth.WORKLOADS[name]
+    lay = wl.layers[li]
+    M, N, K = wl.M, lay.N, lay.K
+    print(f"[case] fullsize asymmetric {name}/{lay.name} M={M} K={K} N={N} "
+          f"kernel={ot.ot_qlinear_plan(M, N, K)}", flush=True)
+    g = _prepare(wl, li, M)
+    _, z, s, inv_s = _check_calibration(wl, g)
+    Wq, sW, zW, bp = ot.fold_weights_asym(torch.from_numpy(g["W"]).cuda(),
+                                          torch.from_numpy(g["b"]).cuda(), wl.w_bits,
+                                          torch.from_numpy(z).cuda(), torch.from_numpy(s).cuda())
+    Y = ot.qlinear_asym(g["Xq_dev"], Wq, sW, zW, bp, wl.a_bits, wl.w_bits)
+    Y2, acc = ot.qlinear_asym(g["Xq_dev"], Wq, sW, zW, bp, wl.a_bits, wl.w_bits, want_acc=True)
+    torch.cuda.synchronize()
+    assert torch.equal(Y, Y2)
+    del Y2
+    rXq = O.quantize_act(g["X"], z, inv_s, wl.a_bits)
+    assert np.array_equal(g["Xq_dev"].cpu().numpy(), rXq)
+    chunk = max(256, CHUNK_BYTES // (8 * M) // 256 * 256)
+    for n0 in range(0, N, chunk):
+        n1 = min(N, n0 + chunk)
+        rWq, rsW, rzW, rbp = O.fold_weights_asym(g["W"][n0:n1], g["b"][n0:n1], z, s, wl.w_bits)
+        assert np.array_equal(Wq[n0:n1].cpu().numpy(), rWq), f"Wq [{n0}, {n1})"
+        assert np.array_equal(sW[n0:n1].cpu().numpy().view(np.uint32), rsW.view(np.uint32))
+        assert np.array_equal(zW[n0:n1].cpu().numpy(), rzW), f"zW [{n0}, {n1})"
+        assert_fp32_within_ulps(bp[n0:n1].cpu().numpy(), rbp, 1)
+        racc = O.int_gemm_asym(rXq, rWq, rzW)
+        assert np.array_equal(acc[:, n0:n1].cpu().numpy(), racc), f"acc [{n0}, {n1})"
+        assert_fp16_close(Y[:, n0:n1].cpu().numpy(), O.epilogue(racc, rsW, rbp),
+                          f"Y [{n0}, {n1})")
+        del racc
+        print(f"  channels [{n0}, {n1}) of {N} match", flush=True)
+
+
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("name,li", [("opt13b_w6a6", 1), ("opt13b_w6a6", 3)])
+def test_prefill_per_token_layer_every_element(name, li):
+    wl = synth.WORKLOADS[name]
+    lay = wl.layers[li]
+    M, N, K = wl.M, lay.N, lay.K
+    print(f"[case] fullsize per-token {name}/{lay.name} M={M} K={K} N={N} "
+          f"kernel={ot.ot_qlinear_plan(M, N, K)}", flush=True)
+    W = synth.weight(wl, li)
+    b = synth.bias(wl, li)
+    X = synth.activations(wl, li, M)
+    Xq, sX = ot.quantize_act_per_token(torch.from_numpy(X).cuda(), wl.a_bits)
+    Wq, sW, bp = ot.fold_weights_per_token(torch.from_numpy(W).cuda(), torch.from_numpy(b).cuda(),
+                                           None, wl.w_bits)
+    Y = ot.qlinear_per_token(Xq, Wq, sX, sW, bp, wl.a_bits, wl.w_bits)
+    Y2, acc = ot.qlinear_per_token(Xq, Wq, sX, sW, bp, wl.a_bits, wl.w_bits, want_acc=True)
+    torch.cuda.synchronize()
+    assert torch.equal(Y, Y2)
+    del Y2
+    rXq, rsX = O.quantize_act_per_token(X, wl.a_bits)
+    assert np.array_equal(Xq.cpu().numpy(), rXq)
+    assert np.array_equal(sX.cpu().numpy().view(np.uint32), rsX.view(np.uint32))
+    chunk = max(256, CHUNK_BYTES // (8 * M) // 256 * 256)
+    for n0 in range(0, N, chunk):
+        n1 = min(N, n0 + chunk)
+        rWq, rsW, rbp = O.fold_weights_per_token(W[n0:n1], b[n0:n1], None, wl.w_bits)
+        assert np.array_equal(Wq[n0:n1].cpu().numpy(), rWq), f"Wq [{n0}, {n1})"
+        assert np.array_equal(sW[n0:n1].cpu().numpy().view(np.uint32), rsW.view(np.uint32))
+        assert_fp32_within_ulps(bp[n0:n1].cpu().numpy(), rbp, 1)
+        racc = O.int_gemm(rXq, rWq)
+        assert np.array_equal(acc[:, n0:n1].cpu().numpy(), racc), f"acc [{n0}, {n1})"
+        assert_fp16_close(Y[:, n0:n1].cpu().numpy(), O.epilogue_per_token(racc, rsX, rsW, rbp),
+                          f"Y [{n0}, {n1})")
+        del racc
+        print(f"  channels [{n0}, {n1}) of {N} match", flush=True)
