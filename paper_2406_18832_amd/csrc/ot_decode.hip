@@ -72,14 +72,61 @@ __device__ __forceinline__ int swz_rows(int r) {
   else return r & 15;
 }
 
+// The epilogue's per-channel scale, bias and zero point (RBW groups of four
+// channels per lane) and per-token scales (MB tokens per lane), loaded at
+// the start of the kernel so that their latency passes during the K loop
+// instead of after it.  Only the waves that run the epilogue (K group 0)
+// load them; a split run has no epilogue.
+template <int RBW, int MB>
+struct EpiParams {
+  float4 s4[RBW], b4[RBW];
+  int4 z4[RBW];
+  float sx[MB];
+};
+
+template <int MB, int RBW, int EPI, bool SPLIT>
+__device__ __forceinline__ void epi_preload(EpiParams<RBW, MB> &ep, const float *__restrict__ sX,
+                                            const int32_t *__restrict__ zW,
+                                            const float *__restrict__ sW,
+                                            const float *__restrict__ bp, int lane, int rg, int kg,
+                                            int nwg0, int M, int N) {
+  if constexpr (!SPLIT) {
+    const int r16 = lane & 15, c4 = lane >> 4;
+    if (kg == 0) {
+#pragma unroll
+      for (int i = 0; i < RBW; ++i)
+        load_epi4<EPI>(sW, bp, zW, (int64_t)nwg0 + (rg * RBW + i) * 16 + 4 * c4, N, ep.s4[i],
+                       ep.b4[i], ep.z4[i]);
+#pragma unroll
+      for (int j = 0; j < MB; ++j) {
+        const int m = j * 16 + r16;
+        ep.sx[j] = (EPI == kEpiToken && m < M) ? sX[m] : 0.f;
+      }
+    }
+  }
+}
+
+// Keeps the compiler from sinking the preloads to their use after the K
+// loop (it emits no instruction; the values are ready by then).
+template <int RBW, int MB>
+__device__ __forceinline__ void epi_pin(EpiParams<RBW, MB> &ep) {
+#pragma unroll
+  for (int i = 0; i < RBW; ++i) {
+    asm volatile("" : "+v"(ep.s4[i].x), "+v"(ep.s4[i].y), "+v"(ep.s4[i].z), "+v"(ep.s4[i].w));
+    asm volatile("" : "+v"(ep.b4[i].x), "+v"(ep.b4[i].y), "+v"(ep.b4[i].z), "+v"(ep.b4[i].w));
+    asm volatile("" : "+v"(ep.z4[i].x), "+v"(ep.z4[i].y), "+v"(ep.z4[i].z), "+v"(ep.z4[i].w));
+  }
+#pragma unroll
+  for (int j = 0; j < MB; ++j) asm volatile("" : "+v"(ep.sx[j]));
+}
+
 // After the K loop: the asymmetric-weight token code sums, the K groups'
 // partial sums added through LDS, then either the epilogue (dequantize,
 // bias, fp16 store) or, split, the run's int32 partial sums.
 template <int MB, int NR, int NK, int RBW, int BKD, int S, int EPI, bool SPLIT>
 __device__ __forceinline__ void decode_finish(
-    int8_t *smem, v4i (&acc)[RBW][MB], int (&rs)[MB], int lane, int rg, int kg, int nwg0,
-    const float *__restrict__ sX, const int32_t *__restrict__ zW, const float *__restrict__ sW,
-    const float *__restrict__ bp, int M, int N, uint16_t *__restrict__ Y,
+    int8_t *smem, v4i (&acc)[RBW][MB], int (&rs)[MB], const EpiParams<RBW, MB> &ep, int lane,
+    int rg, int kg, int nwg0, int M, int N, uint16_t *__restrict__ Y,
     int32_t *__restrict__ acc_out, int32_t *__restrict__ part, int32_t *__restrict__ part_rs) {
   using C = DecodeCfg<MB, NR, NK, RBW, BKD, S>;
   const int r16 = lane & 15, c4 = lane >> 4;
@@ -151,12 +198,11 @@ __device__ __forceinline__ void decode_finish(
 #pragma unroll
   for (int j = 0; j < MB; ++j) {
     const int m = j * 16 + r16;
-    const float sx = (EPI == kEpiToken && m < M) ? sX[m] : 0.f;
 #pragma unroll
     for (int i = 0; i < RBW; ++i) {
       const int64_t n = nwg0 + (rg * RBW + i) * 16 + 4 * c4;
-      store4<EPI>(Y, acc_out, sW, bp, zW, sx, rs[j], m, n, M, N, acc[i][j][0], acc[i][j][1],
-                  acc[i][j][2], acc[i][j][3]);
+      store4_pre<EPI>(Y, acc_out, ep.s4[i], ep.b4[i], ep.z4[i], ep.sx[j], rs[j], m, n, M, N,
+                      acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
     }
   }
 }
@@ -187,6 +233,8 @@ __device__ __forceinline__ void decode_body(
   const __amdgpu_buffer_rsrc_t rw = make_rsrc(Wq + (int64_t)nwg0 * K, (uint32_t)(rows_w * K));
   const __amdgpu_buffer_rsrc_t rx = make_rsrc(Xq, (uint32_t)(M * K));
   const int r16 = lane & 15, c4 = lane >> 4;
+  EpiParams<RBW, MB> ep;
+  epi_preload<MB, RBW, EPI, SPLIT>(ep, sX, zW, sW, bp, lane, rg, kg, nwg0, M, N);
 
   // this wave's j-th load of a stage fills 1 KiB block q = wave*kLoads + j:
   // stage rows q*kRowsPerLoad.. (tokens below kTokRows, then weights)
@@ -255,6 +303,7 @@ __device__ __forceinline__ void decode_body(
   for (int t = 0; t < S - 1; ++t) issue(t);
   wait_vmcnt<(S - 2) * C::kLoads>();
   lds_barrier();
+  epi_pin(ep);
   issue(S - 1);
   for (int st = 0; st < nst; ++st) {
     const int8_t *src = smem + (st % S) * C::kStage;
@@ -284,8 +333,8 @@ __device__ __forceinline__ void decode_body(
   }
   // the ring's last (zero-filling) loads must land before its bytes are reused
   wait_vmcnt<0>();
-  decode_finish<MB, NR, NK, RBW, BKD, S, EPI, SPLIT>(smem, acc, rs, lane, rg, kg, nwg0, sX, zW,
-                                                     sW, bp, M, N, Y, acc_out, part, part_rs);
+  decode_finish<MB, NR, NK, RBW, BKD, S, EPI, SPLIT>(smem, acc, rs, ep, lane, rg, kg, nwg0, M,
+                                                     N, Y, acc_out, part, part_rs);
 }
 
 // Packed weights: wave (rg, kg) loads the micro-tiles of its RBW row blocks
@@ -322,6 +371,8 @@ __device__ __forceinline__ void decode_body_packed(
                                               (uint32_t)groups_w * (uint32_t)KS * kMicroTile);
   const __amdgpu_buffer_rsrc_t rx = make_rsrc(Xq, (uint32_t)(M * K));
   const int r16 = lane & 15, c4 = lane >> 4;
+  EpiParams<RBW, MB> ep;
+  epi_preload<MB, RBW, EPI, SPLIT>(ep, sX, zW, sW, bp, lane, rg, kg, nwg0, M, N);
 
   // token loads: this wave's j-th fills 1 KiB block q = wave*kTL + j of the
   // stage's token rows
@@ -397,6 +448,7 @@ __device__ __forceinline__ void decode_body_packed(
   }
   wait_vmcnt<(S - 2) * kL>();
   lds_barrier();
+  epi_pin(ep);
   issue(S - 1, S - 1);
   const int nrun = (nst + S - 1) / S * S;  // nst >= 1
   int base = 0;
@@ -432,8 +484,8 @@ __device__ __forceinline__ void decode_body_packed(
   } while (base < nrun);
   // the last (zero-filling) loads must land before the ring is reused
   wait_vmcnt<0>();
-  decode_finish<MB, NR, NK, RBW, BKD, S, EPI, SPLIT>(smem, acc, rs, lane, rg, kg, nwg0, sX, zW,
-                                                     sW, bp, M, N, Y, acc_out, part, part_rs);
+  decode_finish<MB, NR, NK, RBW, BKD, S, EPI, SPLIT>(smem, acc, rs, ep, lane, rg, kg, nwg0, M,
+                                                     N, Y, acc_out, part, part_rs);
 }
 
 template <int MB, int NR, int NK, int RBW, int BKD, int S, int EPI, bool PACKED>

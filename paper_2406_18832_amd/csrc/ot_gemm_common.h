@@ -73,17 +73,35 @@ __device__ inline int4 load_zw4(const int32_t *__restrict__ zW, int64_t n, int64
   }
 }
 
-// Writes four consecutive channels n..n+3 of token m.  sx is the token's
-// scale (kEpiToken), rs its code sum (kEpiAsym); acc_out receives the
-// integer sum the epilogue scales.
+// Scale, bias and (asymmetric weights) zero point of the four consecutive
+// channels n..n+3 (zeros past N).
 template <int EPI>
-__device__ inline void store4(uint16_t *__restrict__ Y, int32_t *__restrict__ acc_out,
-                              const float *__restrict__ sW, const float *__restrict__ bp,
-                              const int32_t *__restrict__ zW, float sx, int rs, int64_t m,
-                              int64_t n, int64_t M, int64_t N, int a0, int a1, int a2, int a3) {
+__device__ inline void load_epi4(const float *__restrict__ sW, const float *__restrict__ bp,
+                                 const int32_t *__restrict__ zW, int64_t n, int64_t N, float4 &s4,
+                                 float4 &b4, int4 &z4) {
+  if (n + 3 < N && (N & 3) == 0) {
+    s4 = *reinterpret_cast<const float4 *>(sW + n);
+    b4 = *reinterpret_cast<const float4 *>(bp + n);
+  } else {
+    s4 = make_float4(0.f, 0.f, 0.f, 0.f);
+    b4 = s4;
+    if (n + 0 < N) { s4.x = sW[n + 0]; b4.x = bp[n + 0]; }
+    if (n + 1 < N) { s4.y = sW[n + 1]; b4.y = bp[n + 1]; }
+    if (n + 2 < N) { s4.z = sW[n + 2]; b4.z = bp[n + 2]; }
+    if (n + 3 < N) { s4.w = sW[n + 3]; b4.w = bp[n + 3]; }
+  }
+  z4 = load_zw4<EPI>(zW, n, N);
+}
+
+// Writes four consecutive channels n..n+3 of token m, given their scale,
+// bias and zero point.  sx is the token's scale (kEpiToken), rs its code
+// sum (kEpiAsym); acc_out receives the integer sum the epilogue scales.
+template <int EPI>
+__device__ inline void store4_pre(uint16_t *__restrict__ Y, int32_t *__restrict__ acc_out,
+                                  float4 s4, float4 b4, int4 z4, float sx, int rs, int64_t m,
+                                  int64_t n, int64_t M, int64_t N, int a0, int a1, int a2, int a3) {
   if (m >= M) return;
   if constexpr (EPI == kEpiAsym) {
-    const int4 z4 = load_zw4<EPI>(zW, n, N);
     a0 -= z4.x * rs;
     a1 -= z4.y * rs;
     a2 -= z4.z * rs;
@@ -91,8 +109,6 @@ __device__ inline void store4(uint16_t *__restrict__ Y, int32_t *__restrict__ ac
   }
   const int64_t base = m * N + n;
   if (n + 3 < N && (N & 3) == 0) {
-    const float4 s4 = *reinterpret_cast<const float4 *>(sW + n);
-    const float4 b4 = *reinterpret_cast<const float4 *>(bp + n);
     uint2 o;
     o.x = (uint32_t)dequant_x<EPI>(a0, sx, s4.x, b4.x) |
           ((uint32_t)dequant_x<EPI>(a1, sx, s4.y, b4.y) << 16);
@@ -102,13 +118,28 @@ __device__ inline void store4(uint16_t *__restrict__ Y, int32_t *__restrict__ ac
     if (acc_out) *reinterpret_cast<int4 *>(acc_out + base) = make_int4(a0, a1, a2, a3);
   } else {
     const int a[4] = {a0, a1, a2, a3};
+    const float s[4] = {s4.x, s4.y, s4.z, s4.w}, b[4] = {b4.x, b4.y, b4.z, b4.w};
     for (int i = 0; i < 4; ++i) {
       if (n + i < N) {
-        Y[base + i] = dequant_x<EPI>(a[i], sx, sW[n + i], bp[n + i]);
+        Y[base + i] = dequant_x<EPI>(a[i], sx, s[i], b[i]);
         if (acc_out) acc_out[base + i] = a[i];
       }
     }
   }
+}
+
+// Writes four consecutive channels n..n+3 of token m (loading their scale,
+// bias and zero point).
+template <int EPI>
+__device__ inline void store4(uint16_t *__restrict__ Y, int32_t *__restrict__ acc_out,
+                              const float *__restrict__ sW, const float *__restrict__ bp,
+                              const int32_t *__restrict__ zW, float sx, int rs, int64_t m,
+                              int64_t n, int64_t M, int64_t N, int a0, int a1, int a2, int a3) {
+  if (m >= M) return;
+  float4 s4, b4;
+  int4 z4;
+  load_epi4<EPI>(sW, bp, zW, n, N, s4, b4, z4);
+  store4_pre<EPI>(Y, acc_out, s4, b4, z4, sx, rs, m, n, M, N, a0, a1, a2, a3);
 }
 
 // Sum of the 16 signed bytes of a fragment (one dot-product instruction per
