@@ -1024,6 +1024,9 @@ def main():
         log(f"plain 1 GiB device copy: {result['decode']['hbm_copy_context']['GBps']:.0f} GB/s "
             f"(read + write)")
     pool.shutdown()
+    # provenance: the loaded library's own record of its sources, checked
+    # against the tree this run came from
+    result["library"] = ot.build_info()
     print(json.dumps(result), flush=True)
 
 

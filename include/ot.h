@@ -58,6 +58,16 @@ const char *ot_strerror(int status);
 /* Version of this ABI (bumped on any incompatible change). */
 int ot_abi_version(void);
 
+/* Static description of this build, "key=value" fields separated by ';':
+ *   sources_sha256  SHA-256 of the sources and the release compiler flags
+ *                   it was built from ("unknown" when built without the
+ *                   recipe that computes it), so that a loaded library can
+ *                   be matched against a source tree;
+ *   arch            the GPU architecture of its device code;
+ *   hip             the HIP version it was compiled against.
+ * Never NULL; owned by the library. */
+const char *ot_build_info(void);
+
 /*
  * ot_calibrate -- static min-max calibration and symmetrization factors.
  * Sec. 3.2 (z = (max + min) / 2 per channel, X_hat = X - z) and App. A

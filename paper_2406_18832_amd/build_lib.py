@@ -15,6 +15,7 @@ the binding pointed at it (OT_LIBRARY).
 from __future__ import annotations
 
 import glob
+import hashlib
 import os
 import shutil
 import subprocess
@@ -52,6 +53,25 @@ def sources():
     return sorted(glob.glob(os.path.join(CSRC, "*.hip")))
 
 
+def source_digest() -> str:
+    """SHA-256 over what the library is built from: every csrc/*.hip and
+    csrc/*.h and include/ot.h (each as its path relative to the repository,
+    a zero byte and its contents, in path order), then the release compiler
+    flags (HIPCC_FLAGS; a sanitizer build records the same digest).
+    build() compiles it into the library, which ot_build_info() reports, so
+    a loaded library can be matched against the sources in the tree."""
+    root = os.path.dirname(HERE)
+    files = sorted(glob.glob(os.path.join(CSRC, "*.hip")) + glob.glob(os.path.join(CSRC, "*.h")) +
+                   [os.path.join(root, "include", "ot.h")])
+    h = hashlib.sha256()
+    for f in files:
+        h.update(os.path.relpath(f, root).encode() + b"\0")
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    h.update(" ".join(HIPCC_FLAGS).encode())
+    return h.hexdigest()
+
+
 def asan_runtime() -> str:
     """Path of the compiler's AddressSanitizer runtime (to preload into a
     process that loads the sanitized library)."""
@@ -75,7 +95,8 @@ def build(verbose: bool = False, extra_flags=(), sanitize: bool = False, out: st
     flags = list(HIPCC_FLAGS)
     if sanitize:
         flags = [f for f in flags if f != "-O3"] + ["-O1", *SANITIZE_FLAGS]
-    cmd = [hipcc(), *flags, *extra_flags, *sources(), "-o", tmp]
+    cmd = [hipcc(), *flags, *extra_flags, f'-DOT_SOURCES_SHA256="{source_digest()}"', *sources(),
+           "-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)

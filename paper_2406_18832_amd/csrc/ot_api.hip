@@ -51,6 +51,17 @@ const char *ot_strerror(int status) {
 
 int ot_abi_version(void) { return 1; }
 
+#ifndef OT_SOURCES_SHA256
+#define OT_SOURCES_SHA256 "unknown"
+#endif
+#define OT_STR2(x) #x
+#define OT_STR(x) OT_STR2(x)
+
+const char *ot_build_info(void) {
+  return "sources_sha256=" OT_SOURCES_SHA256 ";arch=gfx950;hip=" OT_STR(HIP_VERSION_MAJOR) "." OT_STR(
+      HIP_VERSION_MINOR) "." OT_STR(HIP_VERSION_PATCH);
+}
+
 ot_status ot_calibrate(const uint16_t *x, int64_t rows, int64_t K, int a_bits, int first,
                        float *minmax, float *z, float *s, float *inv_s, void *stream) {
   if (!x || !minmax || !z || !s || !inv_s) return OT_EINVAL;

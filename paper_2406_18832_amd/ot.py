@@ -45,6 +45,8 @@ def lib() -> ctypes.CDLL:
         L.ot_strerror.argtypes = [c_int]
         L.ot_abi_version.restype = c_int
         L.ot_abi_version.argtypes = []
+        L.ot_build_info.restype = ctypes.c_char_p
+        L.ot_build_info.argtypes = []
         L.ot_calibrate.restype = c_int
         L.ot_calibrate.argtypes = [vp, i64, i64, c_int, c_int, vp, vp, vp, vp, vp]
         L.ot_fold_weights.restype = c_int
@@ -99,6 +101,21 @@ def ot_strerror(code: int) -> str:
 
 def ot_abi_version() -> int:
     return int(lib().ot_abi_version())
+
+
+def ot_build_info() -> str:
+    return lib().ot_build_info().decode()
+
+
+def build_info() -> dict:
+    """ot_build_info()'s fields, the loaded library's path, and whether its
+    sources_sha256 is that of the sources in this tree now (False means the
+    library was built from other sources: rebuild it)."""
+    from . import build_lib
+    info = dict(f.split("=", 1) for f in ot_build_info().split(";") if "=" in f)
+    info["library"] = os.path.relpath(LIB_PATH, os.path.dirname(HERE))
+    info["matches_sources"] = info.get("sources_sha256") == build_lib.source_digest()
+    return info
 
 
 def _check(rc: int, where: str) -> None:

@@ -215,3 +215,14 @@ def test_packed_weights_size_and_argument_checks():
     assert q(0, 8, 32) == ot.OT_OK           # no work
     assert q(4, 8, 32) == ot.OT_EINVAL       # null pointers
     assert q(4, 8, 32, 9) == ot.OT_EINVAL    # bits
+
+
+def test_build_info_names_these_sources():
+    """The loaded library reports the SHA-256 of the sources and flags it was
+    built from; it must be that of the tree under test (a stale build would
+    test other code)."""
+    info = ot.build_info()
+    assert info["arch"] == "gfx950"
+    assert len(info["sources_sha256"]) == 64 and int(info["sources_sha256"], 16) >= 0
+    assert info["hip"].count(".") == 2
+    assert info["matches_sources"], "libot.so was built from other sources: rebuild it"
