@@ -233,7 +233,7 @@ __device__ __forceinline__ void decode_body(
   const __amdgpu_buffer_rsrc_t rw = make_rsrc(Wq + (int64_t)nwg0 * K, (uint32_t)(rows_w * K));
   const __amdgpu_buffer_rsrc_t rx = make_rsrc(Xq, (uint32_t)(M * K));
   const int r16 = lane & 15, c4 = lane >> 4;
-  EpiParams<RBW, MB> ep;
+  EpiParams<RBW, MB> ep{};  // zeros where this wave loads none
   epi_preload<MB, RBW, EPI, SPLIT>(ep, sX, zW, sW, bp, lane, rg, kg, nwg0, M, N);
 
   // this wave's j-th load of a stage fills 1 KiB block q = wave*kLoads + j:
@@ -371,7 +371,7 @@ __device__ __forceinline__ void decode_body_packed(
                                               (uint32_t)groups_w * (uint32_t)KS * kMicroTile);
   const __amdgpu_buffer_rsrc_t rx = make_rsrc(Xq, (uint32_t)(M * K));
   const int r16 = lane & 15, c4 = lane >> 4;
-  EpiParams<RBW, MB> ep;
+  EpiParams<RBW, MB> ep{};  // zeros where this wave loads none
   epi_preload<MB, RBW, EPI, SPLIT>(ep, sX, zW, sW, bp, lane, rg, kg, nwg0, M, N);
 
   // token loads: this wave's j-th fills 1 KiB block q = wave*kTL + j of the
