@@ -755,7 +755,7 @@ static hipError_t decode_tiles(const DecodePlan &p, const int8_t *Xq, const int8
       if (p.rows == 32) OT_TILE(2, 2, 1, 1, 128, 8);
       if (p.rows == 64) OT_TILE(2, 4, 1, 1, 128, 8);
       if (p.rows == 96) OT_TILE(2, 2, 2, 3, 128, 8);
-      OT_TILE(2, 8, 1, 1, 256, 3);
+      OT_TILE(2, 4, 1, 2, 128, 4);
     } else {
       if (p.rows == 32) OT_TILE(2, 2, 4, 1, 256, 4);
       if (p.rows == 64) OT_TILE(2, 4, 2, 1, 256, 4);
