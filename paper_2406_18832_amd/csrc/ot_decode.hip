@@ -766,6 +766,9 @@ static hipError_t decode_tiles(const DecodePlan &p, const int8_t *Xq, const int8
   if constexpr (PACKED) {
     if (p.rows == 32) OT_TILE(4, 2, 4, 1, 256, 4);
     if (p.rows == 64) OT_TILE(4, 4, 2, 1, 256, 4);
+    // over all of K, 2 K groups with 4 stages; the split runs (shorter K)
+    // keep the 4 K groups with 3 stages below
+    if (p.rows == 96 && p.runs == 1) OT_TILE(4, 2, 2, 3, 256, 4);
   } else {
     if (p.rows == 32) OT_TILE(4, 2, 4, 1, 256, 3);
     if (p.rows == 64) OT_TILE(4, 4, 2, 1, 256, 3);
