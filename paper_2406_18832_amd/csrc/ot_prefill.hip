@@ -50,6 +50,12 @@ struct PrefillCfg {
   static_assert(kTN % 32 == 0 && kTM % 32 == 0, "MFMA tiling");
   static_assert(S >= 2 && (S - 2) * kLoads <= 63, "vmcnt range");
   static_assert(S * kStage <= 160 * 1024, "LDS");
+  // the workgroup's fp16 output tile, staged whole in LDS by the epilogue
+  // when it fits beside (after) the ring's bytes in the 160 KiB
+  static constexpr int kOutBytes = BN * BM * 2;
+  static constexpr int kSmem = kOutBytes > S * kStage && kOutBytes <= 160 * 1024
+                                   ? kOutBytes
+                                   : S * kStage;
 };
 
 // LDS swizzle of an operand tile [rows][BK]: chunk c (16 bytes) of row r is
@@ -342,10 +348,11 @@ __device__ __forceinline__ void prefill_body(
     return;
   }
   // Dequantize into a wave-private fp16 staging tile in the now idle LDS
-  // ring, then write whole token rows with 16-byte stores.  The tile holds
-  // kSlab token rows by kTN channels: the wave's whole block when every
-  // wave's block fits the ring, else 32 tokens (one register block g) at a
-  // time.  In LDS the 8-byte unit u (4 channels) of staging row r sits at
+  // (the ring, and past it up to 160 KiB where the workgroup's output tile
+  // needs more), then write whole token rows with 16-byte stores.  The tile
+  // holds kSlab token rows by kTN channels: the wave's whole block when every
+  // wave's block fits, else 32 tokens (one register block g) at a time.
+  // In LDS the 8-byte unit u (4 channels) of staging row r sits at
   // unit u ^ h(r), h(r) < kSwz: the lanes that write one register group (32
   // tokens, same channels) then spread over the banks (h(r) = r mod 16 for
   // 128-byte rows, (r / 2) mod 8 for 320-byte rows, each checked
@@ -353,11 +360,11 @@ __device__ __forceinline__ void prefill_body(
   constexpr int kUnits = C::kTN / 4;                       // 8-byte units per row
   constexpr int kSwz = (kUnits % 16 == 0) ? 16 : 8;         // XOR group of the swizzle
   constexpr int kCpr = C::kTN / 8;                          // 16-byte chunks per row
-  constexpr bool kWhole = C::kWaves * C::kTM * C::kTN * 2 <= S * C::kStage;
+  constexpr bool kWhole = C::kWaves * C::kTM * C::kTN * 2 <= C::kSmem;
   constexpr int kSlab = kWhole ? C::kTM : 32;               // token rows per staging pass
   constexpr int kSlabG = kSlab / 32;                        // register blocks per pass
   static_assert(kUnits % kSwz == 0, "the swizzle permutes whole groups of units");
-  static_assert(C::kWaves * kSlab * C::kTN * 2 <= S * C::kStage, "staging tile fits the ring");
+  static_assert(C::kWaves * kSlab * C::kTN * 2 <= C::kSmem, "staging tile fits the LDS");
   static_assert((kSlab * kCpr) % 64 == 0, "row pass covers the slab in whole wave passes");
   auto stage_swz = [](int r) { return kSwz == 16 ? (r & 15) : ((r >> 1) & 7); };
   __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): this wave's last reads
@@ -459,7 +466,7 @@ __global__ __launch_bounds__(64 * WN * WM, OCC) void qgemm_prefill_kernel(
     int M, int N, int K, uint16_t *__restrict__ Y, int32_t *__restrict__ acc_out, int tiles_m,
     int tiles_n, int group_m) {
   __shared__ __attribute__((aligned(1024)))
-  int8_t smem[S * PrefillCfg<BN, BM, BK, WN, WM, S>::kStage];
+  int8_t smem[PrefillCfg<BN, BM, BK, WN, WM, S>::kSmem];
   prefill_body<BN, BM, BK, WN, WM, S, EPI, MPL>(smem, Xq, Wq, sX, zW, sW, bp, M, N, K, Y, acc_out,
                                            tiles_m, tiles_n, group_m);
 }
@@ -512,7 +519,8 @@ static double prefill_cost(int64_t M, int64_t N, int64_t K, int bn, int bm, int 
 // Four tile shapes, each one workgroup of 8 waves per CU with a 2-stage
 // ring of BK = 128:
 //   256 (channels) x 256 (tokens), waves 4 x 2 of 64 x 128 (128 KiB of LDS);
-//   320 x 256, waves 2 x 4 of 160 x 64 (144 KiB): lets layers whose tile
+//   320 x 256, waves 2 x 4 of 160 x 64 (a 144 KiB ring in 160 KiB, which
+//     holds the epilogue's whole output tile): lets layers whose tile
 //     count leaves the last pass over the CUs mostly empty fill whole passes
 //     (4096 tokens by 5120 or 15360 channels: 256 and 768 tiles against 320
 //     and 960 of 256 x 256);
