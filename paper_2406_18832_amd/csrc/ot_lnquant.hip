@@ -347,13 +347,14 @@ using namespace detail;
 hipError_t launch_ln_quantize_act(const uint16_t *h, int64_t M, int64_t K, const uint16_t *gamma,
                                   const uint16_t *beta, float eps, int qa, const float *z,
                                   const float *inv_s, int8_t *Xq, hipStream_t st) {
-  // one row per workgroup, 4 chunks of 8 channels per thread up to
-  // K = 2048 and 8 beyond (a workgroup of at most 1024 threads covers
-  // K = 65536); measured on K = 768 ... 32768 against 2 to 32 chunks per
-  // thread, 1 or 2 rows per workgroup and two launch bounds (8 chunks is
-  // 10 % faster than 4 at K = 4096 and within 2 % of the best from 3072 to
-  // 9216)
-  if (K <= 2048) return launch_lnq<4, 1>(h, M, K, gamma, beta, eps, qa, z, inv_s, Xq, st);
+  // one row per workgroup, 6 chunks of 8 channels per thread up to
+  // K = 49152 (a workgroup of at most 1024 threads) and 8 beyond (up to
+  // K = 65536).  Measured on 8 shapes (K = 2048 ... 12288, 1024 to 8192
+  // rows) against 3 to 8 chunks per thread and 1, 2 or 4 rows per
+  // workgroup: 6 chunks and one row is 10 % faster than 8 chunks over the
+  // shapes (its fewer registers keep more rows in flight per CU), the
+  // fastest at 4 of them and within 9 % of the fastest at every one
+  if (K <= 6 * 8 * 1024) return launch_lnq<6, 1>(h, M, K, gamma, beta, eps, qa, z, inv_s, Xq, st);
   return launch_lnq<8, 1>(h, M, K, gamma, beta, eps, qa, z, inv_s, Xq, st);
 }
 

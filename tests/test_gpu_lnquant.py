@@ -64,11 +64,12 @@ def _run(H, gamma, beta, eps, a_bits, z, inv_s):
     return Xq.cpu().numpy()
 
 
-# widths on both sides of the 16384 / 32768 kernel-configuration boundaries,
-# ragged against the 8-channel chunks and the 64-thread waves
+# widths on both sides of the 49152 kernel-configuration boundary (6 and 8
+# chunks of 8 channels per thread), ragged against the 8-channel chunks and
+# the 64-thread waves, up to the widest row
 SHAPES = [(1, 16), (3, 768), (17, 1040), (130, 512), (4, 2048), (7, 2064), (64, 4096),
           (9, 5120), (5, 16384),
-          (2, 16400), (3, 32768), (2, 32784), (1, 65536)]
+          (2, 16400), (3, 32768), (2, 32784), (2, 49152), (2, 49168), (1, 65536)]
 
 
 @pytest.mark.parametrize("M,K", SHAPES)
