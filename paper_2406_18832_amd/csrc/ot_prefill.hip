@@ -449,11 +449,7 @@ __device__ __forceinline__ void prefill_body(
       }
     }
   };
-  // (the asymmetric flavour keeps one, checked copy: with its zero points
-  // and code sums a second copy spills registers on the 320 x 256 tile)
-  if constexpr (EPI == kEpiAsym)
-    epilogue(BoolC<false>{});
-  else if (n0 + BN <= N && m0 + BM <= M && (N & 7) == 0)
+  if (n0 + BN <= N && m0 + BM <= M && (N & 7) == 0)
     epilogue(BoolC<true>{});
   else
     epilogue(BoolC<false>{});
