@@ -50,8 +50,9 @@ struct PrefillCfg {
   static_assert(kTN % 32 == 0 && kTM % 32 == 0, "MFMA tiling");
   static_assert(S >= 2 && (S - 2) * kLoads <= 63, "vmcnt range");
   static_assert(S * kStage <= 160 * 1024, "LDS");
-  // the workgroup's fp16 output tile, staged whole in LDS by the epilogue
-  // when it fits beside (after) the ring's bytes in the 160 KiB
+  // the workgroup's fp16 output tile, which the epilogue stages whole in the
+  // idle ring: where it is larger than the ring, the workgroup takes LDS for
+  // it (up to the 160 KiB a workgroup can have)
   static constexpr int kOutBytes = BN * BM * 2;
   static constexpr int kSmem = kOutBytes > S * kStage && kOutBytes <= 160 * 1024
                                    ? kOutBytes
