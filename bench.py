@@ -70,6 +70,12 @@ def parse():
     p.add_argument("--quality", action="store_true",
                    help="only run the symmetrization ablation / bit-width sweep of output error "
                         "against float64 (one JSON line)")
+    p.add_argument("--helper-probe", action="store_true",
+                   help="launch the quantizer and the fused LayerNorm on the OPT-13B shapes "
+                        "(for counter runs)")
+    p.add_argument("--helper-traffic", metavar="DIR",
+                   help="print the quantizer's and fused LayerNorm's HBM-side traffic from "
+                        "counter runs under DIR (host only)")
     p.add_argument("--decode-probe", action="store_true",
                    help="only run each decode-regime linear once per token count (for counter runs)")
     p.add_argument("--counter-summary", metavar="DIR",
@@ -687,6 +693,85 @@ def copy_probe(torch):
     print(json.dumps({"copy_probe_bytes_read": n, "copy_probe_bytes_written": n, "launches": 3}))
 
 
+# (label, rows, channels, kernel) of the helper probe's launches, three each
+HELPER_PROBE = [("ot_quantize_act, qkv/out/fc1 input", 4096, 5120, "quantize_act_kernel"),
+                ("ot_quantize_act, fc2 input", 4096, 20480, "quantize_act_kernel"),
+                ("ot_ln_quantize_act, qkv/fc1 LayerNorm", 4096, 5120, "ln_quantize_kernel")]
+
+
+def helper_probe(torch, ot, synth, wl):
+    """The activation quantizer and the fused LayerNorm on the OPT-13B W6A6
+    shapes, three launches each, with a 1 GiB buffer written between launches
+    so that each reads its input from HBM rather than the last-level cache."""
+    flush = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+    K1 = wl.layers[0].K
+    gamma, beta = (torch.from_numpy(a).cuda() for a in synth.ln_params(wl, 0))
+    for label, M, K, kern in HELPER_PROBE:
+        X = torch.randn(M, K, device="cuda").half()
+        z = torch.zeros(K, device="cuda")
+        inv_s = torch.full((K,), 4.0, device="cuda")
+        Xq = torch.empty((M, K), dtype=torch.int8, device="cuda")
+        for _ in range(3):
+            flush.fill_(0)
+            if kern == "ln_quantize_kernel":
+                assert K == K1
+                ot.ot_ln_quantize_act(X, gamma, beta, 1e-5, wl.a_bits, z, inv_s, Xq)
+            else:
+                ot.ot_quantize_act(X, wl.a_bits, z, inv_s, Xq)
+        torch.cuda.synchronize()
+    print(json.dumps({"helper_probe": [[lab, M, K] for lab, M, K, _ in HELPER_PROBE],
+                      "launches_each": 3}))
+
+
+def helper_traffic(d):
+    """Markdown table of the helper probe's HBM-side bytes per launch, from
+    FETCH_SIZE and WRITE_SIZE runs over `bench.py --helper-probe` (under
+    d/helper_fetch, d/helper_write) scaled by the same counters on the 1 GiB
+    copy (d/copy_fetch, d/copy_write).  Host only."""
+    n_copy = 1 << 30
+    factors = {}
+    for c, sub in (("FETCH_SIZE", "copy_fetch"), ("WRITE_SIZE", "copy_write")):
+        disp = _per_dispatch(_counter_rows(os.path.join(d, sub), c), "copyBuffer")
+        kib = [v for _, v in disp if v > 0.5 * n_copy / 1024 / 4]
+        factors[c] = n_copy / 1024 / float(np.median(kib))
+    got, ns = {}, {}
+    for c, sub in (("FETCH_SIZE", "helper_fetch"), ("WRITE_SIZE", "helper_write")):
+        rows = _counter_rows(os.path.join(d, sub), c)
+        q = [v for _, v in _per_dispatch(rows, "quantize_act_kernel")]
+        ln = [v for _, v in _per_dispatch(rows, "ln_quantize_kernel")]
+        if len(q) != 6 or len(ln) != 3:
+            raise SystemExit(f"{sub}: {len(q)} quantizer and {len(ln)} LayerNorm dispatches, "
+                             "expected 6 and 3")
+        got[c] = [q[:3], q[3:], ln]
+        for r in rows:  # each dispatch's own duration, both runs
+            if "quantize_act_kernel" in r["Kernel_Name"] or "ln_quantize_kernel" in r["Kernel_Name"]:
+                ns[(sub, int(r["Dispatch_Id"]))] = (r["Kernel_Name"],
+                                                    int(r["End_Timestamp"]) - int(r["Start_Timestamp"]))
+    dur = [[], [], []]
+    for sub in ("helper_fetch", "helper_write"):
+        ds = [v for k, v in sorted(ns.items()) if k[0] == sub]
+        qs = [t for n, t in ds if "quantize_act_kernel" in n]
+        dur[0] += qs[:3]
+        dur[1] += qs[3:]
+        dur[2] += [t for n, t in ds if "ln_quantize_kernel" in n]
+    out = [f"Calibration on the 1 GiB copy: FETCH_SIZE factor {factors['FETCH_SIZE']:.3f}, "
+           f"WRITE_SIZE factor {factors['WRITE_SIZE']:.3f} (bytes = KiB x 1024 x factor).", "",
+           "| Launch | rows x channels | read bytes | written bytes | algorithmic read / written | "
+           "read / algorithmic | written / algorithmic | us per launch (median of 6, under the "
+           "profiler) | algorithmic GB/s |",
+           "|---|---|---|---|---|---|---|---|---|"]
+    for i, (label, M, K, kern) in enumerate(HELPER_PROBE):
+        rd = float(np.mean(got["FETCH_SIZE"][i])) * 1024 * factors["FETCH_SIZE"]
+        wr = float(np.mean(got["WRITE_SIZE"][i])) * 1024 * factors["WRITE_SIZE"]
+        params = 12 * K if kern == "ln_quantize_kernel" else 8 * K  # gamma, beta, z, 1/s
+        a_rd, a_wr = 2 * M * K + params, M * K
+        us = float(np.median(dur[i])) / 1e3
+        out.append(f"| {label} | {M} x {K} | {rd / 1e6:.1f} MB | {wr / 1e6:.1f} MB | "
+                   f"{a_rd / 1e6:.1f} / {a_wr / 1e6:.1f} MB | {rd / a_rd:.3f} | {wr / a_wr:.3f} | "
+                   f"{us:.1f} | {(a_rd + a_wr) / (us * 1e-6) / 1e9:.0f} |")
+    print("\n".join(out))
+
+
 def hbm_copy_context(torch, iters=10):
     """A plain 1 GiB device-to-device copy (torch's), for context: bytes read
     plus written per second."""
@@ -895,6 +980,9 @@ def main():
     if args.counter_summary:
         counter_summary(args.counter_summary, args.workload, args.decode_workload)
         return
+    if args.helper_traffic:
+        helper_traffic(args.helper_traffic)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the quantized linear "
               "is single-device here and no multi-GPU path is built.", file=sys.stderr)
@@ -905,6 +993,9 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     if args.copy_probe:
         copy_probe(torch)
+        return
+    if args.helper_probe:
+        helper_probe(torch, ot, synth, synth.WORKLOADS[args.workload])
         return
     if args.decode_probe:
         ot.lib()

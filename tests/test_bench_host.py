@@ -1,6 +1,7 @@
 """Host-side logic of bench.py that needs no GPU: the prefill GEMM's fetch
 floor under its tile schedule, the rule that reports recorded HBM traffic
-only for the kernel source it was taken on, and the one-GPU guard."""
+only for the kernel source it was taken on, the helper kernels' traffic
+summary, and the one-GPU guard."""
 import json
 import os
 import subprocess
@@ -66,3 +67,43 @@ def test_more_than_one_gpu_is_refused():
                          capture_output=True, text=True, timeout=300)
     assert out.returncode != 0
     assert "one GPU" in out.stdout + out.stderr
+
+
+def _counter_csv(path, counter, dispatches):
+    """A rocprofv3 counter_collection.csv with one row per (dispatch, kernel,
+    value, start, end)."""
+    path.mkdir(parents=True)
+    lines = ['"Dispatch_Id","Kernel_Name","Grid_Size","Counter_Name","Counter_Value",'
+             '"Start_Timestamp","End_Timestamp"']
+    for d, name, value, t0, t1 in dispatches:
+        lines.append(f'{d},"{name}",1024,"{counter}",{value},{t0},{t1}')
+    (path / "p_counter_collection.csv").write_text("\n".join(lines) + "\n")
+
+
+def test_helper_traffic_table(tmp_path, capsys):
+    """The helper probe's summary scales each dispatch's FETCH_SIZE and
+    WRITE_SIZE by the copy's factors and sets them against the algorithmic
+    bytes of its shape: made-up counters equal to those bytes give ratios of
+    exactly 1."""
+    gib_kib = (1 << 30) / 1024
+    _counter_csv(tmp_path / "copy_fetch", "FETCH_SIZE",
+                 [(1, "__amd_rocclr_copyBuffer", gib_kib / 2, 0, 100)])
+    _counter_csv(tmp_path / "copy_write", "WRITE_SIZE",
+                 [(1, "__amd_rocclr_copyBuffer", gib_kib, 0, 100)])
+    fetch, write, d = [], [], 1
+    for label, M, K, kern in bench.HELPER_PROBE:
+        rd = 2 * M * K + (12 if kern == "ln_quantize_kernel" else 8) * K
+        for _ in range(3):
+            fetch.append((d, f"ot::detail::{kern}<6>", rd / 1024 / 2, 0, 10_000))
+            write.append((d, f"ot::detail::{kern}<6>", M * K / 1024, 0, 10_000))
+            d += 1
+    _counter_csv(tmp_path / "helper_fetch", "FETCH_SIZE", fetch)
+    _counter_csv(tmp_path / "helper_write", "WRITE_SIZE", write)
+    bench.helper_traffic(str(tmp_path))
+    out = capsys.readouterr().out
+    rows = [line for line in out.splitlines() if line.startswith("| ot_")]
+    assert len(rows) == 3
+    for row in rows:
+        cells = [c.strip() for c in row.strip("|").split("|")]
+        assert cells[5] == "1.000" and cells[6] == "1.000", row
+        assert cells[7] == "10.0", row
